@@ -1,0 +1,63 @@
+"""The seeded input generator: reproducibility, distributions, bf16 rounding."""
+from fractions import Fraction
+
+import numpy as np
+import torch
+
+import synth
+from synth import workloads
+
+
+def test_bf16_rounding_matches_torch():
+    rng = np.random.default_rng(0)
+    x = np.concatenate([rng.standard_normal(100000).astype(np.float32),
+                        np.array([1.0, -1.0, 0.0, 1.00390625, 1.01171875,
+                                  3.3895314e38, 1e-40], np.float32)])
+    # ties: 1 + 2^-8 rounds to even (1.0), 1 + 3*2^-8 rounds up
+    ours = synth.f32_to_bf16_bits(x)
+    theirs = torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(ours, theirs)
+    back = synth.bf16_bits_to_f32(ours)
+    assert np.array_equal(back, torch.from_numpy(ours.view(np.int16)).view(torch.bfloat16).float().numpy())
+
+
+def test_tail_is_a_slice_of_the_prefix():
+    shape = synth.Shape(2, 4, 16, 8, "bf16")
+    full = synth.tokens(9, 1, 2, 0, 300, shape)
+    tail = synth.tokens(9, 1, 2, 171, 300, shape)
+    for name in ("q", "k", "v", "g", "beta"):
+        assert np.array_equal(getattr(full, name)[171:], getattr(tail, name))
+    other = synth.tokens(9, 2, 2, 171, 300, shape)
+    assert not np.array_equal(other.k, tail.k)
+
+
+def test_distributions():
+    shape = synth.Shape(2, 4, 64, 32, "f32")
+    t = synth.tokens(1, 0, 0, 0, 640, shape, gate_scale=0.1)
+    assert np.allclose(np.linalg.norm(t.k.astype(np.float64), axis=-1), 1.0, atol=1e-6)
+    assert np.allclose(np.linalg.norm(t.q.astype(np.float64), axis=-1), 1.0, atol=1e-6)
+    assert np.all(t.g < 0) and np.all(t.g > -2.0)
+    assert np.all((t.beta > 0) & (t.beta < 1))
+    # mean softplus(N(0,1)) ~ 0.806
+    assert abs(float(-t.g.mean()) / 0.1 - 0.806) < 0.05
+    assert abs(float(t.v.std()) - 1.0) < 0.05
+
+
+def test_pack_offsets_and_exact_values():
+    shape = synth.Shape(1, 2, 8, 8, "bf16")
+    seqs = [synth.tokens(5, 0, i, 0, n, shape) for i, n in enumerate([3, 0, 65])]
+    p = synth.pack(seqs)
+    assert p.cu_seqlens.tolist() == [0, 3, 3, 68]
+    assert p.cu_seqlens.dtype == np.int32
+    ex = p.exact()
+    assert ex["k"].dtype == np.float64
+    assert np.array_equal(ex["k"].astype(np.float32), synth.bf16_bits_to_f32(p.k))
+
+
+def test_workload3_draw_is_fixed():
+    d = workloads.workload3_draw()
+    assert len(d) == 16
+    assert all(m in (8192, 16384, 32768) for m, _, _ in d)
+    assert all(Fraction(1, 20) <= r <= Fraction(1, 10) for _, r, _ in d)
+    assert all(128 <= s <= 2048 for _, _, s in d)
+    assert d == workloads.workload3_draw()
