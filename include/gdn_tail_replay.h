@@ -1,0 +1,170 @@
+/*
+ * gdn_tail_replay.h -- C ABI of the MI355X (gfx950) Gated DeltaNet
+ * tail-replay library (libgdn_tailreplay.so).
+ *
+ * The operation (paper Section 2, Eq. 1; Section 3, Eq. 2).  For every packed
+ * sequence n and value head h, with key/query head kh = h / (Hv / Hk), the
+ * gated delta rule
+ *     S_t = S_{t-1} alpha_t (I - beta_t k_t k_t^T) + beta_t v_t k_t^T,
+ *     alpha_t = exp(g_t),
+ * is applied token by token.  The state is stored transposed, M = S^T, as a
+ * d_k x d_v row-major fp32 matrix (d_v fastest):
+ *     M_t = alpha_t M_{t-1} + k_t (beta_t (v_t - alpha_t M_{t-1}^T k_t))^T.
+ * Independent Tail-Replay (Eq. 2) starts from a zero state at the first token
+ * of the replayed tail and keeps the state after its last token.  The forward
+ * call continues from a given state and also emits o_t = scale * S_t q_t
+ * (computed after the update of token t).
+ *
+ * Layouts (all buffers C-contiguous, tokens packed varlen, token-major):
+ *     q, k     [T, Hk, d_k]        qkv_dtype
+ *     v, o     [T, Hv, d_v]        qkv_dtype
+ *     g, beta  [T, Hv]             fp32; g = log alpha <= 0, beta in [0, 1]
+ *     state    [N, Hv, d_k, d_v]   fp32, M = S^T
+ *     cu_seqlens [N + 1]           int32 token offsets, cu[0] = 0, cu[N] = T
+ *
+ * Conventions
+ *   - Pointers are device pointers unless their name ends in _host.
+ *   - The caller owns every buffer, including the workspace.  The library
+ *     never allocates, never synchronises and never copies between host and
+ *     device; every call only enqueues kernels on `stream` (a hipStream_t,
+ *     NULL = the null stream) and returns.
+ *   - Validation happens on the host, from cu_seqlens_host, before anything is
+ *     enqueued; a rejected call launches nothing and writes nothing.  The
+ *     caller guarantees that cu_seqlens (device) holds the same values.
+ *   - g <= 0 and beta in [0, 1] are assumed, not checked.  q and k are used as
+ *     given (normalising them is the caller's job).
+ *   - Zero-length sequences are allowed: tail replay writes a zero state,
+ *     forward writes state_in (or zeros when state_in is NULL).
+ *   - Inputs are never written.  state_out may alias state_in only when the two
+ *     pointers are equal.  Calls that share a workspace must be ordered on one
+ *     stream.
+ *   - Reentrant; the only global state is a thread-local error message.
+ */
+#ifndef GDN_TAIL_REPLAY_H
+#define GDN_TAIL_REPLAY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  GDN_OK = 0,
+  GDN_ERR_NULL_ARG = 1,     /* a required pointer is NULL                    */
+  GDN_ERR_BAD_SHAPE = 2,    /* head counts / dimensions inconsistent         */
+  GDN_ERR_BAD_SEQLENS = 3,  /* cu_seqlens_host not 0-based non-decreasing    */
+  GDN_ERR_UNSUPPORTED = 4,  /* valid but not built: d not in {64,128}, dtype */
+  GDN_ERR_WORKSPACE = 5,    /* workspace NULL or smaller than required       */
+  GDN_ERR_HIP = 6           /* a HIP runtime call failed; see gdn_last_error */
+} gdn_status;
+
+typedef enum { GDN_F32 = 0, GDN_BF16 = 1 } gdn_dtype;
+
+typedef struct {
+  int32_t num_seqs;     /* N >= 0                                            */
+  int32_t num_k_heads;  /* Hk >= 1: heads of q and k                         */
+  int32_t num_v_heads;  /* Hv >= 1: heads of v, g, beta, o, state; Hv % Hk == 0 */
+  int32_t d_k;          /* key head dimension, 64 or 128                     */
+  int32_t d_v;          /* value head dimension, 64 or 128                   */
+  int32_t qkv_dtype;    /* gdn_dtype of q, k, v and o                        */
+  float scale;          /* output scale: o_t = scale * S_t q_t               */
+} gdn_shape;
+
+/*
+ * Workspace bytes needed by gdn_tail_replay (with_outputs = 0) or
+ * gdn_chunk_forward (with_outputs = 1) for this shape and these sequence
+ * lengths.  Writes *bytes; returns a validation status (nothing enqueued).
+ */
+gdn_status gdn_workspace_size(const gdn_shape* shape,
+                              const int32_t* cu_seqlens_host,
+                              int32_t with_outputs, size_t* bytes);
+
+/*
+ * Independent Tail-Replay (paper Section 3, Eq. 2): for each sequence (one
+ * replayed tail of a matched prefix, packed by cu_seqlens) and value head,
+ * start from the zero state and apply Eq. 1 to every token; write the state
+ * after the sequence's last token to state_out [N, Hv, d_k, d_v].
+ *   k [T,Hk,d_k], v [T,Hv,d_v] (qkv_dtype); g, beta [T,Hv] fp32.
+ * workspace: device memory of at least gdn_workspace_size(..., 0) bytes,
+ * 256-byte aligned; its contents on entry do not matter.
+ */
+gdn_status gdn_tail_replay(const gdn_shape* shape,
+                           const int32_t* cu_seqlens_host,
+                           const int32_t* cu_seqlens,
+                           const void* k, const void* v,
+                           const float* g, const float* beta,
+                           float* state_out,
+                           void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/*
+ * Chunked forward over new tokens (the suffix after a rebuilt state, paper
+ * Section 3): start each (sequence, value head) from state_in (NULL = zero
+ * state), apply Eq. 1 to every token, write o_t = scale * S_t q_t to
+ * o [T, Hv, d_v] (qkv_dtype) and, unless state_out is NULL, the final state
+ * to state_out [N, Hv, d_k, d_v] (may equal state_in).
+ * workspace: at least gdn_workspace_size(..., 1) bytes, 256-byte aligned.
+ */
+gdn_status gdn_chunk_forward(const gdn_shape* shape,
+                             const int32_t* cu_seqlens_host,
+                             const int32_t* cu_seqlens,
+                             const void* q, const void* k, const void* v,
+                             const float* g, const float* beta,
+                             const float* state_in,
+                             void* o, float* state_out,
+                             void* workspace, size_t workspace_bytes,
+                             void* stream);
+
+/*
+ * Profiling variants: identical work and results, plus stage timing.  The
+ * library enqueues its kernels in gdn_num_stages(with_outputs) stages; before
+ * stage i it records stage_events[i] (a hipEvent_t created by the caller) on
+ * `stream`, and after the last stage it records stage_events[num_stages].
+ * num_events must be gdn_num_stages(...) + 1.  Stages that have nothing to do
+ * still record their event, so every event is recorded on every call.
+ */
+gdn_status gdn_tail_replay_profiled(const gdn_shape* shape,
+                                    const int32_t* cu_seqlens_host,
+                                    const int32_t* cu_seqlens,
+                                    const void* k, const void* v,
+                                    const float* g, const float* beta,
+                                    float* state_out,
+                                    void* workspace, size_t workspace_bytes,
+                                    void* stream,
+                                    void* const* stage_events, int32_t num_events);
+
+gdn_status gdn_chunk_forward_profiled(const gdn_shape* shape,
+                                      const int32_t* cu_seqlens_host,
+                                      const int32_t* cu_seqlens,
+                                      const void* q, const void* k, const void* v,
+                                      const float* g, const float* beta,
+                                      const float* state_in,
+                                      void* o, float* state_out,
+                                      void* workspace, size_t workspace_bytes,
+                                      void* stream,
+                                      void* const* stage_events, int32_t num_events);
+
+/* Number of kernel stages a call enqueues, and the name of stage i. */
+int32_t gdn_num_stages(int32_t with_outputs);
+const char* gdn_stage_name(int32_t with_outputs, int32_t stage);
+
+/*
+ * Replay budget of the paper (Section 3): k = ceil(r * m) for a ratio
+ * r = ratio_num / ratio_den, in exact integer arithmetic.  Returns -1 when
+ * m < 0, ratio_num < 0, ratio_den <= 0 or the product overflows.
+ */
+int64_t gdn_replay_len(int64_t m, int64_t ratio_num, int64_t ratio_den);
+
+/* Static description of a status code. */
+const char* gdn_status_string(gdn_status status);
+
+/* Detail of the last failed call on this thread ("" if none). */
+const char* gdn_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GDN_TAIL_REPLAY_H */

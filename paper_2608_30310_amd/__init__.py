@@ -1,0 +1,14 @@
+"""MI355X-native Gated DeltaNet tail replay (Tail-Replay, arXiv 2608.30310).
+
+On a prefix-cache hit of a hybrid model, every GDN recurrent state is rebuilt
+by replaying only the last r tokens of the matched prefix from a zero state
+(paper Section 3, Eq. 2); the same chunked kernels then continue over the new
+suffix and emit its outputs.  The work runs in hand-written HIP kernels for
+gfx950 behind the C ABI declared in ``include/gdn_tail_replay.h``; this
+package is a thin binding of that library.
+"""
+from .binding import (GDNError, LIB_PATH, chunk_forward, load_library, replay_len,
+                      stage_names, tail_replay, workspace_size)
+
+__all__ = ["GDNError", "LIB_PATH", "chunk_forward", "load_library", "replay_len",
+           "stage_names", "tail_replay", "workspace_size"]

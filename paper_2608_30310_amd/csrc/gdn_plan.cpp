@@ -1,0 +1,83 @@
+// Host-side validation and workspace planning (see gdn_plan.h).
+#include "gdn_plan.h"
+
+#include <cmath>
+#include <limits>
+
+namespace gdn {
+namespace {
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool supported_dim(int32_t d) { return d == 64 || d == 128; }
+
+}  // namespace
+
+gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_outputs,
+                     Plan* plan, std::string* err) {
+  if (!shape) { *err = "shape is NULL"; return GDN_ERR_NULL_ARG; }
+  if (!plan) { *err = "plan is NULL"; return GDN_ERR_NULL_ARG; }
+  const int32_t N = shape->num_seqs, hk = shape->num_k_heads, hv = shape->num_v_heads;
+  if (N < 0) { *err = "num_seqs must be >= 0"; return GDN_ERR_BAD_SHAPE; }
+  if (hk < 1 || hv < 1) { *err = "head counts must be >= 1"; return GDN_ERR_BAD_SHAPE; }
+  if (hv % hk != 0) {
+    *err = "num_v_heads must be a multiple of num_k_heads";
+    return GDN_ERR_BAD_SHAPE;
+  }
+  if (shape->d_k < 1 || shape->d_v < 1) { *err = "head dimensions must be >= 1"; return GDN_ERR_BAD_SHAPE; }
+  if (!supported_dim(shape->d_k) || !supported_dim(shape->d_v)) {
+    *err = "d_k and d_v must each be 64 or 128";
+    return GDN_ERR_UNSUPPORTED;
+  }
+  if (shape->qkv_dtype != GDN_F32 && shape->qkv_dtype != GDN_BF16) {
+    *err = "qkv_dtype must be GDN_F32 or GDN_BF16";
+    return GDN_ERR_UNSUPPORTED;
+  }
+  if (!std::isfinite(shape->scale)) { *err = "scale must be finite"; return GDN_ERR_BAD_SHAPE; }
+  if (hv > 65535) { *err = "num_v_heads must be <= 65535"; return GDN_ERR_UNSUPPORTED; }
+  if (!cu) { *err = "cu_seqlens_host is NULL"; return GDN_ERR_NULL_ARG; }
+  if (cu[0] != 0) { *err = "cu_seqlens_host[0] must be 0"; return GDN_ERR_BAD_SEQLENS; }
+
+  int64_t chunks = 0;
+  int32_t max_chunks = 0;
+  for (int32_t n = 0; n < N; ++n) {
+    const int64_t len = static_cast<int64_t>(cu[n + 1]) - cu[n];
+    if (len < 0) { *err = "cu_seqlens_host must be non-decreasing"; return GDN_ERR_BAD_SEQLENS; }
+    const int64_t c = (len + kChunk - 1) / kChunk;
+    chunks += c;
+    if (c > max_chunks) max_chunks = static_cast<int32_t>(c);
+  }
+  const int64_t T = cu[N];
+  // Units of work are addressed with 32-bit grid indices.
+  if (chunks > std::numeric_limits<int32_t>::max() / 2) {
+    *err = "too many chunks";
+    return GDN_ERR_UNSUPPORTED;
+  }
+  if (static_cast<int64_t>(N) * hv * 4 > std::numeric_limits<int32_t>::max()) {
+    *err = "num_seqs * num_v_heads too large";
+    return GDN_ERR_UNSUPPORTED;
+  }
+
+  Plan p;
+  p.total_tokens = T;
+  p.num_chunks = chunks;
+  p.max_chunks = max_chunks;
+  p.with_outputs = with_outputs;
+  const size_t ch = static_cast<size_t>(chunks);
+  size_t off = 0;
+  p.off_seq_chunk = off;
+  off = align_up(off + sizeof(int32_t) * (static_cast<size_t>(N) + 1));
+  p.off_chunk_info = off;
+  off = align_up(off + 2 * sizeof(int32_t) * ch);
+  p.off_T = off;
+  off = align_up(off + sizeof(float) * ch * hv * kChunk * kChunk);
+  p.off_G = off;
+  off = align_up(off + sizeof(float) * ch * hv * kChunk);
+  p.off_P = off;
+  if (with_outputs) off = align_up(off + sizeof(float) * ch * hv * kChunk * kChunk);
+  p.bytes = off;
+  *plan = p;
+  return GDN_OK;
+}
+
+}  // namespace gdn

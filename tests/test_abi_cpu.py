@@ -1,0 +1,164 @@
+"""The C ABI on the host: symbols, validation paths, replay-length rule (no GPU).
+
+Calls here only take paths that the library rejects on the host before it
+touches a device: every case carries at least one invalid argument.  Device
+pointers are placeholders that are never dereferenced; on a machine with a GPU
+these cases are skipped so no placeholder can ever reach a kernel.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+import oracle
+import paper_2608_30310_amd as gdn
+from paper_2608_30310_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gdn_tail_replay.h")
+
+FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gdn_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("gdn_tail_replay", "gdn_chunk_forward", "gdn_workspace_size",
+                 "gdn_replay_len", "gdn_status_string", "gdn_last_error"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(binding.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), f"{name} declared in the header but not exported"
+
+
+def _shape(**kw):
+    base = dict(num_seqs=1, num_k_heads=16, num_v_heads=32, d_k=128, d_v=128,
+                qkv_dtype=binding.GDN_BF16, scale=1.0)
+    base.update(kw)
+    return binding.GDNShape(**base)
+
+
+def _cu(vals):
+    arr = (ctypes.c_int32 * len(vals))(*vals)
+    return arr
+
+
+def _ws_size(shape, cu, fwd=0):
+    lib = gdn.load_library()
+    out = ctypes.c_size_t(0)
+    st = lib.gdn_workspace_size(ctypes.byref(shape) if shape is not None else None,
+                                ctypes.cast(cu, ctypes.c_void_p) if cu is not None else None,
+                                fwd, ctypes.byref(out))
+    return st, out.value
+
+
+@pytest.mark.parametrize("kw,cu,status", [
+    (dict(num_k_heads=3), [0, 10], 2),              # Hv % Hk != 0
+    (dict(num_k_heads=0), [0, 10], 2),
+    (dict(num_seqs=-1), [0], 2),
+    (dict(d_k=96), [0, 10], 4),                     # unsupported head dim
+    (dict(d_v=256), [0, 10], 4),
+    (dict(qkv_dtype=7), [0, 10], 4),
+    (dict(scale=float("nan")), [0, 10], 2),
+    (dict(), [1, 10], 3),                           # does not start at 0
+    (dict(num_seqs=2), [0, 10, 5], 3),              # decreasing
+])
+def test_workspace_size_rejects(kw, cu, status):
+    st, _ = _ws_size(_shape(**kw), _cu(cu))
+    assert st == status
+    assert gdn.load_library().gdn_last_error().decode()
+
+
+def test_workspace_size_null_args():
+    assert _ws_size(None, _cu([0, 1]))[0] == 1
+    assert _ws_size(_shape(), None)[0] == 1
+
+
+def test_workspace_size_values():
+    # 13 chunks of 64 for 819 tokens; T matrices 13*32*64*64*4 bytes dominate
+    st, n = _ws_size(_shape(), _cu([0, 819]))
+    assert st == 0
+    assert n >= 13 * 32 * 64 * 64 * 4
+    st, nf = _ws_size(_shape(), _cu([0, 819]), 1)
+    assert st == 0 and nf >= n + 13 * 32 * 64 * 64 * 4
+    st, z = _ws_size(_shape(num_seqs=0), _cu([0]))
+    assert st == 0 and z < 1024
+    assert gdn.workspace_size(1, 16, 32, 128, 128, [0, 819]) == n
+
+
+needs_no_gpu = pytest.mark.skipif(torch.cuda.is_available(),
+                                  reason="placeholder pointers are only used without a GPU")
+
+
+@needs_no_gpu
+@pytest.mark.parametrize("case", ["null_k", "null_state", "small_ws", "null_ws", "misaligned_ws",
+                                  "bad_seqlens", "null_cu_dev", "bad_heads"])
+def test_tail_replay_rejects_before_launch(case):
+    lib = gdn.load_library()
+    shape = _shape(num_k_heads=3) if case == "bad_heads" else _shape()
+    cu_host = _cu([0, 5, 3] if case == "bad_seqlens" else [0, 100])
+    if case == "bad_seqlens":
+        shape = _shape(num_seqs=2)
+    _, need = _ws_size(_shape(), _cu([0, 100]))
+    ws = None if case == "null_ws" else ctypes.c_void_p(0x10000 + (8 if case == "misaligned_ws" else 0))
+    ws_bytes = need - 1 if case == "small_ws" else need
+    st = lib.gdn_tail_replay(ctypes.byref(shape), ctypes.cast(cu_host, ctypes.c_void_p),
+                             None if case == "null_cu_dev" else FAKE,
+                             None if case == "null_k" else FAKE, FAKE, FAKE, FAKE,
+                             None if case == "null_state" else FAKE, ws, ws_bytes, None)
+    want = {"null_k": 1, "null_state": 1, "small_ws": 5, "null_ws": 5, "misaligned_ws": 5,
+            "bad_seqlens": 3, "null_cu_dev": 1, "bad_heads": 2}[case]
+    assert st == want, lib.gdn_last_error().decode()
+
+
+@needs_no_gpu
+@pytest.mark.parametrize("case", ["null_q", "null_o", "overlap", "small_ws"])
+def test_chunk_forward_rejects_before_launch(case):
+    lib = gdn.load_library()
+    shape = _shape(num_seqs=2)
+    cu_host = _cu([0, 50, 100])
+    _, need = _ws_size(shape, cu_host, 1)
+    state_bytes = 2 * 32 * 128 * 128 * 4
+    s_in = ctypes.c_void_p(0x100000)
+    s_out = ctypes.c_void_p(0x100000 + (state_bytes // 2 if case == "overlap" else 2 * state_bytes))
+    st = lib.gdn_chunk_forward(ctypes.byref(shape), ctypes.cast(cu_host, ctypes.c_void_p), FAKE,
+                               None if case == "null_q" else FAKE, FAKE, FAKE, FAKE, FAKE,
+                               s_in, None if case == "null_o" else FAKE, s_out,
+                               ctypes.c_void_p(0x20000),
+                               need - 256 if case == "small_ws" else need, None)
+    want = {"null_q": 1, "null_o": 1, "overlap": 2, "small_ws": 5}[case]
+    assert st == want, lib.gdn_last_error().decode()
+
+
+def test_status_strings():
+    lib = gdn.load_library()
+    for code in range(7):
+        assert lib.gdn_status_string(code).decode().startswith("GDN_")
+
+
+def test_replay_len_matches_the_oracle():
+    lib = gdn.load_library()
+    for m in (0, 1, 63, 2048, 8192, 16384, 32768, 31366, 31847):
+        for ratio in ("0.05", "0.1", "1/3", "0.0723", "1"):
+            assert gdn.replay_len(m, ratio) == oracle.replay_len(m, ratio)
+    assert gdn.replay_len(8192, "0.1") == 820     # the paper's ceiling
+    assert lib.gdn_replay_len(-1, 1, 10) == -1
+    assert lib.gdn_replay_len(10, 1, 0) == -1
+    assert lib.gdn_replay_len(2 ** 62, 4, 1) == -1
+    with pytest.raises(TypeError):
+        gdn.replay_len(10, 0.1)
+
+
+def test_binding_raises_gdn_error():
+    with pytest.raises(gdn.GDNError):
+        binding._check(2)

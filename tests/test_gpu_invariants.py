@@ -1,0 +1,167 @@
+"""Properties of the HIP path that hold at any size (needs an MI355X).
+
+Bitwise: replaying the whole prefix equals the forward's final state (Eq. 2
+with k = m), a varlen batch equals per-sequence calls, grouped heads equal the
+matching single-head problem, repeated runs are identical, an empty replay is
+exactly zero (the zero-only baseline), in-place state update equals the
+out-of-place one.  Within tolerance: splitting a sequence at any token and
+handing the state over equals one call.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2608_30310_amd as gdn
+import synth
+from tests.gpu_util import STATE_TOL, OUTPUT_TOL, device_inputs, oracle_run, state_err, to_f64
+
+pytestmark = pytest.mark.gpu
+
+SHAPE = synth.Shape(hk=2, hv=4, dk=128, dv=128, dtype="bf16")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    gdn.load_library()
+
+
+def _seq(seq, n, start=0, shape=SHAPE, gate_scale=0.1):
+    return synth.tokens(200, 0, seq, start, start + n, shape, gate_scale)
+
+
+def test_replay_of_whole_prefix_is_full_prefill_bitwise():
+    p = synth.pack([_seq(0, 333)])
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    _, st_f = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    assert torch.equal(st, st_f)
+
+
+def test_varlen_batch_equals_separate_calls_bitwise():
+    lens = [130, 0, 64, 1, 257]
+    seqs = [_seq(i, n) for i, n in enumerate(lens)]
+    p = synth.pack(seqs)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    o, st_f = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                                state_in=st)
+    for i, s in enumerate(seqs):
+        xi = device_inputs(synth.pack([s]))
+        sti = gdn.tail_replay(xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"], xi["cu_host"])
+        assert torch.equal(st[i], sti[0])
+        oi, sfi = gdn.chunk_forward(xi["q"], xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"],
+                                    xi["cu_host"], state_in=sti)
+        a, b = int(p.cu_seqlens[i]), int(p.cu_seqlens[i + 1])
+        assert torch.equal(o[a:b], oi)
+        assert torch.equal(st_f[i], sfi[0])
+
+
+def test_grouped_heads_equal_single_head_problems_bitwise():
+    p = synth.pack([_seq(0, 200)])
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    o, _ = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    grp = SHAPE.hv // SHAPE.hk
+    for h in range(SHAPE.hv):
+        kh = h // grp
+        sl = lambda t, a: t[:, a:a + 1].contiguous()
+        sth = gdn.tail_replay(sl(x["k"], kh), sl(x["v"], h), sl(x["g"], h), sl(x["beta"], h),
+                              x["cu"], x["cu_host"])
+        oh, _ = gdn.chunk_forward(sl(x["q"], kh), sl(x["k"], kh), sl(x["v"], h), sl(x["g"], h),
+                                  sl(x["beta"], h), x["cu"], x["cu_host"])
+        assert torch.equal(st[:, h], sth[:, 0])
+        assert torch.equal(o[:, h], oh[:, 0])
+
+
+def test_repeated_runs_are_identical():
+    p = synth.pack([_seq(0, 700), _seq(1, 90)])
+    x = device_inputs(p)
+    ref_st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"]).clone()
+    ref_o, _ = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"],
+                                 x["cu_host"], state_in=ref_st)
+    ref_o = ref_o.clone()
+    for _ in range(10):
+        st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+        o, _ = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"],
+                                 x["cu_host"], state_in=st)
+        assert torch.equal(st, ref_st) and torch.equal(o, ref_o)
+
+
+def test_zero_length_replay_is_the_zero_only_baseline():
+    p = synth.pack([_seq(0, 0), _seq(1, 0)], SHAPE)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    assert st.shape == (2, SHAPE.hv, SHAPE.dk, SHAPE.dv)
+    assert torch.count_nonzero(st).item() == 0
+    s0 = torch.randn_like(st)
+    o, s1 = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                              state_in=s0)
+    assert o.numel() == 0 and torch.equal(s1, s0)
+
+
+def test_no_sequences_is_a_no_op():
+    p = synth.pack([], SHAPE)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    assert st.shape == (0, SHAPE.hv, SHAPE.dk, SHAPE.dv)
+
+
+def test_in_place_state_update_matches_out_of_place():
+    p = synth.pack([_seq(0, 150), _seq(1, 70)])
+    x = device_inputs(p)
+    s0 = torch.randn(2, SHAPE.hv, SHAPE.dk, SHAPE.dv, device="cuda") * 0.2
+    o1, s1 = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                               state_in=s0)
+    s_inplace = s0.clone()
+    o2, s2 = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                               state_in=s_inplace, state_out=s_inplace)
+    assert s2.data_ptr() == s_inplace.data_ptr()
+    assert torch.equal(o1, o2) and torch.equal(s1, s2)
+
+
+@pytest.mark.parametrize("split", [1, 37, 64, 100, 191])
+def test_state_hand_off_at_any_token(split):
+    n = 256
+    whole = synth.pack([_seq(0, n)])
+    head = synth.pack([_seq(0, split)])
+    rest = synth.pack([_seq(0, n - split, start=split)])
+    xw, xh, xr = device_inputs(whole), device_inputs(head), device_inputs(rest)
+    o, s = gdn.chunk_forward(xw["q"], xw["k"], xw["v"], xw["g"], xw["beta"], xw["cu"],
+                             xw["cu_host"])
+    oh, sh = gdn.chunk_forward(xh["q"], xh["k"], xh["v"], xh["g"], xh["beta"], xh["cu"],
+                               xh["cu_host"])
+    orr, sr = gdn.chunk_forward(xr["q"], xr["k"], xr["v"], xr["g"], xr["beta"], xr["cu"],
+                                xr["cu_host"], state_in=sh)
+    assert state_err(to_f64(sr), to_f64(s)) <= STATE_TOL / 10
+    o_cat = torch.cat([oh, orr])
+    rel = (o_cat.float() - o.float()).norm() / o.float().norm()
+    assert rel.item() <= OUTPUT_TOL / 5
+    # and both agree with the oracle
+    _, want = oracle_run(whole)
+    assert state_err(to_f64(sr), want) <= STATE_TOL
+
+
+@pytest.mark.parametrize("gate_scale", [0.02, 0.5, 2.0])
+def test_gate_scales(gate_scale):
+    p = synth.pack([_seq(0, 300, gate_scale=gate_scale)])
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    _, want = oracle_run(p)
+    assert state_err(to_f64(st), want) <= STATE_TOL
+
+
+def test_adversarial_repeated_keys():
+    """Identical keys in a chunk (A has all-equal entries): the triangular solve
+    must stay accurate."""
+    shape = synth.Shape(hk=1, hv=1, dk=64, dv=64, dtype="f32")
+    t = synth.tokens(201, 0, 0, 0, 192, shape)
+    t.k[:] = t.k[0]
+    t.beta[:] = 0.999
+    t.g[:] = -1e-4
+    p = synth.pack([t])
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    _, want = oracle_run(p)
+    assert state_err(to_f64(st), want) <= STATE_TOL
