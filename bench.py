@@ -180,7 +180,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32",
+        "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": f"one GDN layer, Hk=16 Hv=32 d_k=d_v=128 bf16 q/k/v; "
                                f"prefix 8192, tail replay r={r} from zero + {s}-token suffix "

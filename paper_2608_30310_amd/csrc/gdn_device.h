@@ -1,0 +1,227 @@
+// Device helpers for the gfx950 GDN kernels: bf16 conversion, hi/lo splitting,
+// MFMA wrappers and the k-slot permutation shared by all scan contractions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace gdn {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((__vector_size__(4 * sizeof(float))));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------- bf16
+__device__ __forceinline__ uint16_t f2bf(float x) {
+  // round to nearest, ties to even (finite values)
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+__device__ __forceinline__ float bf2f(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// x = hi + lo with hi = bf16(x), lo = bf16(x - hi): |x - hi - lo| <= 2^-16 |x|.
+__device__ __forceinline__ void split_bf16(float x, uint16_t& hi, uint16_t& lo) {
+  hi = f2bf(x);
+  lo = f2bf(x - bf2f(hi));
+}
+
+// A fragment split into bf16 high and low parts.
+struct Frag {
+  bf16x8 hi;
+  bf16x8 lo;
+};
+
+// Split of eight values with the hardware bf16 conversion: hi = bf16(x),
+// lo = bf16(x - hi).  The conversion's rounding only moves weight between hi
+// and lo; the pair still carries x to ~2^-16 relative.
+__device__ __forceinline__ Frag split8(const float (&v)[8]) {
+  f32x8 x;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) x[j] = v[j];
+  Frag f;
+  f.hi = __builtin_convertvector(x, bf16x8);
+  const f32x8 back = __builtin_convertvector(f.hi, f32x8);
+  f.lo = __builtin_convertvector(x - back, bf16x8);
+  return f;
+}
+
+// Reinterpret two 8-byte halves (4 bf16 each) as one operand.
+__device__ __forceinline__ bf16x8 join_halves(u32x2 a, u32x2 b) {
+  u32x4 u = u32x4{a.x, a.y, b.x, b.y};
+  return __builtin_bit_cast(bf16x8, u);
+}
+
+// ---------------------------------------------------------------- MFMA
+// D(16x16) += A(16x32) B(32x16), bf16 inputs, fp32 accumulate.  Lane l supplies
+// A[l%16][8(l/16)+j] and B[8(l/16)+j][l%16] for j = 0..7 and holds
+// D[4(l/16)+i][l%16] for i = 0..3.
+__device__ __forceinline__ f32x4 mma(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// exact bf16 A times split B: two passes.
+__device__ __forceinline__ f32x4 mma_x2(bf16x8 a, const Frag& b, f32x4 c) {
+  c = mma(a, b.hi, c);
+  return mma(a, b.lo, c);
+}
+
+// split A times split B: three passes (the lo*lo term, ~2^-16 relative, is dropped).
+__device__ __forceinline__ f32x4 mma_x3(const Frag& a, const Frag& b, f32x4 c) {
+  c = mma(a.hi, b.hi, c);
+  c = mma(a.hi, b.lo, c);
+  return mma(a.lo, b.hi, c);
+}
+
+// A operand that is exact bf16 (SPLIT = false) or split (SPLIT = true).
+template <bool SPLIT>
+__device__ __forceinline__ f32x4 mma_a(const Frag& a, const Frag& b, f32x4 c) {
+  if constexpr (SPLIT) return mma_x3(a, b, c);
+  else return mma_x2(a.hi, b, c);
+}
+
+// ---------------------------------------------------------------- k-slot permutation
+// Within a 32-wide k step, MFMA slot 8g + j (g = lane/16, j = 0..7) is mapped to
+// contraction index 4g + j for j < 4 and 16 + 4g + (j - 4) for j >= 4.  With this
+// order the accumulator that lane (g, c) holds for two consecutive 16-row tiles,
+// rows 4g..4g+3 of each, is exactly its B operand for the next contraction over
+// those 32 rows, so results chain through registers without a shuffle.
+__device__ __forceinline__ int kperm(int g, int j) { return (j < 4) ? 4 * g + j : 16 + 4 * g + (j - 4); }
+
+// B fragment over rows [32kk, 32kk + 32) from two accumulator tiles (rows
+// 32kk..32kk+15 and 32kk+16..32kk+31), optionally scaled per element.
+__device__ __forceinline__ Frag chain_frag(const f32x4& lo_tile, const f32x4& hi_tile) {
+  float v[8];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    v[j] = lo_tile[j];
+    v[4 + j] = hi_tile[j];
+  }
+  return split8(v);
+}
+
+__device__ __forceinline__ f32x4 zero4() {
+  f32x4 z = {0.f, 0.f, 0.f, 0.f};
+  return z;
+}
+
+// ---------------------------------------------------------------- element access
+// Raw storage bits of an element (bf16 bits or fp32 bits) and their value.
+__device__ __forceinline__ uint32_t load_bits(const float* p, int64_t i) { return __float_as_uint(p[i]); }
+__device__ __forceinline__ uint32_t load_bits(const uint16_t* p, int64_t i) { return p[i]; }
+template <typename TIn>
+__device__ __forceinline__ float bits_value(uint32_t b) {
+  if constexpr (sizeof(TIn) == 2) return __uint_as_float(b << 16);
+  else return __uint_as_float(b);
+}
+__device__ __forceinline__ float load_elt(const float* p, int64_t i) { return p[i]; }
+__device__ __forceinline__ float load_elt(const uint16_t* p, int64_t i) { return bf2f(p[i]); }
+__device__ __forceinline__ void store_elt(float* p, int64_t i, float x) { p[i] = x; }
+__device__ __forceinline__ void store_elt(uint16_t* p, int64_t i, float x) { p[i] = f2bf(x); }
+
+// A-operand fragment in kperm order from an LDS row: elements c0..c0+3 and
+// c0+16..c0+19 (two 8-byte reads), c0 = 32 kk + 4 (lane / 16).
+__device__ __forceinline__ bf16x8 perm_frag(const uint16_t* p) {
+  return join_halves(*reinterpret_cast<const u32x2*>(p), *reinterpret_cast<const u32x2*>(p + 16));
+}
+
+// ---------------------------------------------------------------- chunk row tiles
+// The 64 chunk rows of one head of a token-major [T, H, D] tensor, held as
+// 16-byte vectors spread over a 256-thread workgroup.  `base` points at row 0
+// of the head; row i starts `row_stride` elements later.  Rows at or past
+// `rows` (1 <= rows <= 64) read as zero: the loads themselves are unconditional
+// (clamped to the last valid row) so no load waits behind a branch, and the
+// padding is applied when the tile is written to LDS.
+template <typename TIn, int D>
+struct RowTile {
+  static constexpr int kVecPerRow = D * static_cast<int>(sizeof(TIn)) / 16;
+  static constexpr int kElemsPerVec = 16 / static_cast<int>(sizeof(TIn));
+  static constexpr int kPerThread = 64 * kVecPerRow / 256;
+  u32x4 d[kPerThread];
+  int rows;
+
+  __device__ __forceinline__ static int row(int tid, int m) { return (tid + 256 * m) / kVecPerRow; }
+  __device__ __forceinline__ static int col(int tid, int m) {
+    return ((tid + 256 * m) % kVecPerRow) * kElemsPerVec;
+  }
+  __device__ __forceinline__ void load(const TIn* __restrict__ base, int64_t row_stride, int nrows,
+                                       int tid) {
+    rows = nrows;
+#pragma unroll
+    for (int m = 0; m < kPerThread; ++m) {
+      const int i = min(row(tid, m), nrows - 1);
+      d[m] = *reinterpret_cast<const u32x4*>(base + i * row_stride + col(tid, m));
+    }
+  }
+  __device__ __forceinline__ u32x4 get(int tid, int m) const {
+    return row(tid, m) < rows ? d[m] : u32x4{0u, 0u, 0u, 0u};
+  }
+};
+
+// Element j of a 16-byte vector as float (bf16 or fp32 payload).
+template <typename TIn>
+__device__ __forceinline__ float vec_elt(const u32x4& u, int j) {
+  if constexpr (sizeof(TIn) == 2) {
+    const uint32_t w = (j < 2) ? u.x : (j < 4) ? u.y : (j < 6) ? u.z : u.w;
+    return __uint_as_float((j & 1) ? (w & 0xFFFF0000u) : (w << 16));
+  } else {
+    const uint32_t w = (j == 0) ? u.x : (j == 1) ? u.y : (j == 2) ? u.z : u.w;
+    return __uint_as_float(w);
+  }
+}
+
+// Writes a tile row-major into LDS as bf16: dst[p][row][col], p = 0 for the
+// value (bf16 input) or the high part, p = 1 for the low part (fp32 input).
+template <typename TIn, int D, int NL, int PITCH>
+__device__ __forceinline__ void store_rows(uint16_t (*dst)[64][PITCH], const RowTile<TIn, D>& t,
+                                           int tid) {
+#pragma unroll
+  for (int m = 0; m < RowTile<TIn, D>::kPerThread; ++m) {
+    const int i = RowTile<TIn, D>::row(tid, m), c = RowTile<TIn, D>::col(tid, m);
+    const u32x4 val = t.get(tid, m);
+    if constexpr (sizeof(TIn) == 2) {
+      *reinterpret_cast<u32x4*>(&dst[0][i][c]) = val;
+    } else {
+      uint16_t hi[4], lo[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) split_bf16(vec_elt<TIn>(val, j), hi[j], lo[j]);
+      *reinterpret_cast<u32x2*>(&dst[0][i][c]) =
+          u32x2{hi[0] | (uint32_t(hi[1]) << 16), hi[2] | (uint32_t(hi[3]) << 16)};
+      *reinterpret_cast<u32x2*>(&dst[NL - 1][i][c]) =
+          u32x2{lo[0] | (uint32_t(lo[1]) << 16), lo[2] | (uint32_t(lo[3]) << 16)};
+    }
+  }
+}
+
+// Writes a tile transposed into LDS as bf16: dst[p][col][row].
+template <typename TIn, int D, int NL, int PITCH>
+__device__ __forceinline__ void store_cols(uint16_t (*dst)[D][PITCH], const RowTile<TIn, D>& t,
+                                           int tid) {
+  constexpr int E = RowTile<TIn, D>::kElemsPerVec;
+#pragma unroll
+  for (int m = 0; m < RowTile<TIn, D>::kPerThread; ++m) {
+    const int i = RowTile<TIn, D>::row(tid, m), c = RowTile<TIn, D>::col(tid, m);
+    const u32x4 val = t.get(tid, m);
+#pragma unroll
+    for (int j = 0; j < E; ++j) {
+      if constexpr (sizeof(TIn) == 2) {
+        const uint32_t w = (j < 2) ? val.x : (j < 4) ? val.y : (j < 6) ? val.z : val.w;
+        dst[0][c + j][i] = static_cast<uint16_t>((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+      } else {
+        uint16_t hi, lo;
+        split_bf16(vec_elt<TIn>(val, j), hi, lo);
+        dst[0][c + j][i] = hi;
+        dst[NL - 1][c + j][i] = lo;
+      }
+    }
+  }
+}
+
+}  // namespace gdn

@@ -1,6 +1,7 @@
 // Host-side validation and workspace planning (see gdn_plan.h).
 #include "gdn_plan.h"
 
+#include <algorithm>
 #include <cmath>
 #include <limits>
 
@@ -38,13 +39,14 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   if (!cu) { *err = "cu_seqlens_host is NULL"; return GDN_ERR_NULL_ARG; }
   if (cu[0] != 0) { *err = "cu_seqlens_host[0] must be 0"; return GDN_ERR_BAD_SEQLENS; }
 
-  int64_t chunks = 0;
+  int64_t chunks = 0, slots = 0;
   int32_t max_chunks = 0;
   for (int32_t n = 0; n < N; ++n) {
     const int64_t len = static_cast<int64_t>(cu[n + 1]) - cu[n];
     if (len < 0) { *err = "cu_seqlens_host must be non-decreasing"; return GDN_ERR_BAD_SEQLENS; }
     const int64_t c = (len + kChunk - 1) / kChunk;
     chunks += c;
+    if (c > 0) slots = std::max(slots, chunk_slot(cu[n], n) + c);
     if (c > max_chunks) max_chunks = static_cast<int32_t>(c);
   }
   const int64_t T = cu[N];
@@ -58,23 +60,28 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
     return GDN_ERR_UNSUPPORTED;
   }
 
+  if (slots > std::numeric_limits<int32_t>::max() / 2) {
+    *err = "too many chunk slots";
+    return GDN_ERR_UNSUPPORTED;
+  }
+
   Plan p;
   p.total_tokens = T;
   p.num_chunks = chunks;
+  p.num_slots = slots;
   p.max_chunks = max_chunks;
   p.with_outputs = with_outputs;
-  const size_t ch = static_cast<size_t>(chunks);
+  const size_t recs = static_cast<size_t>(slots) * hv;
+  p.k_record = k_record_bytes(shape->d_k, with_outputs, shape->qkv_dtype == GDN_F32);
   size_t off = 0;
-  p.off_seq_chunk = off;
-  off = align_up(off + sizeof(int32_t) * (static_cast<size_t>(N) + 1));
-  p.off_chunk_info = off;
-  off = align_up(off + 2 * sizeof(int32_t) * ch);
+  p.off_K = off;
+  off = align_up(off + p.k_record * static_cast<size_t>(slots) * hk);
   p.off_T = off;
-  off = align_up(off + sizeof(float) * ch * hv * kChunk * kChunk);
-  p.off_G = off;
-  off = align_up(off + sizeof(float) * ch * hv * kChunk);
+  off = align_up(off + kTRecordBytes * recs);
+  p.off_S = off;
+  off = align_up(off + kSRecordBytes * recs);
   p.off_P = off;
-  if (with_outputs) off = align_up(off + sizeof(float) * ch * hv * kChunk * kChunk);
+  if (with_outputs) off = align_up(off + kPRecordBytes * recs);
   p.bytes = off;
   *plan = p;
   return GDN_OK;

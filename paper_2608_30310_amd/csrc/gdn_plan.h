@@ -13,18 +13,45 @@ namespace gdn {
 constexpr int kChunk = 64;        // tokens per chunk
 constexpr size_t kAlign = 256;    // alignment of every workspace region
 
+// Chunk j of sequence n uses workspace slot cu[n] / 64 + n + j.  The map is
+// injective (ceil(len / 64) <= len / 64 + 1), so kernels find their records
+// from cu_seqlens alone; at most N slots stay unused.
+inline int64_t chunk_slot(int64_t seq_start, int64_t seq) { return seq_start / kChunk + seq; }
+
+// Workspace records.  A fragment is one MFMA operand for a whole wave: 64 lanes
+// x 8 bf16 = 1 KiB.  Per (slot, key head), the K record holds the chunk's keys
+// as A operands for K M (4 row tiles x d_k/32 k steps), for K^T Delta
+// (d_k/16 row tiles x 2 k steps) and, with outputs, the queries for Q M; fp32
+// inputs store a high and a low bf16 part.  Per (slot, value head), T and P
+// keep their six nonzero fragments (hi + lo) and S the per-row scalars.
+constexpr size_t kFragBytes = 1024;
+constexpr int kTFrags = 6;                                   // nonzero (row tile, k step) pairs
+constexpr size_t kTRecordBytes = 2 * kTFrags * kFragBytes;   // T, split hi/lo
+constexpr size_t kPRecordBytes = kTRecordBytes;              // P, split hi/lo
+constexpr size_t kSRecordBytes = 5 * 64 * 4;                 // per-row fp32 scalars
+
+constexpr int ka_frags(int dk) { return 4 * (dk / 32); }     // K as A for K M
+constexpr int kt_frags(int dk) { return (dk / 16) * 2; }     // K^T as A for K^T Delta
+constexpr int k_record_frags(int dk, bool outputs) {          // per bf16 part
+  return ka_frags(dk) + kt_frags(dk) + (outputs ? ka_frags(dk) : 0);
+}
+constexpr size_t k_record_bytes(int dk, bool outputs, bool split) {
+  return static_cast<size_t>(k_record_frags(dk, outputs)) * (split ? 2 : 1) * kFragBytes;
+}
+
 // Where each region lives inside the caller's workspace, and the launch sizes.
 struct Plan {
   int64_t total_tokens = 0;
   int64_t num_chunks = 0;         // sum over sequences of ceil(len / 64)
+  int64_t num_slots = 0;          // 1 + largest slot index in use (0 if none)
   int32_t max_chunks = 0;         // longest sequence, in chunks
   bool with_outputs = false;
+  size_t k_record = 0;            // bytes of one K record
   // byte offsets into the workspace
-  size_t off_seq_chunk = 0;       // int32 [N + 1]: first chunk of each sequence
-  size_t off_chunk_info = 0;      // int32x2 [num_chunks]: (first token, length)
-  size_t off_T = 0;               // fp32 [num_chunks, Hv, 64, 64]: (I + A)^-1
-  size_t off_G = 0;               // fp32 [num_chunks, Hv, 64]: in-chunk cumulative log-gate
-  size_t off_P = 0;               // fp32 [num_chunks, Hv, 64, 64]: scale * (Q K^T) * decay (outputs only)
+  size_t off_K = 0;               // [num_slots, Hk] K records
+  size_t off_T = 0;               // [num_slots, Hv] T = (I + A)^-1 fragments
+  size_t off_S = 0;               // [num_slots, Hv] row scalars
+  size_t off_P = 0;               // [num_slots, Hv] P fragments (outputs only)
   size_t bytes = 0;               // total workspace size
 };
 
