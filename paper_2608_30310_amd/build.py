@@ -31,6 +31,9 @@ def build(verbose: bool = False) -> str:
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            # packed fp32 instructions stay off on this target
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+           # MFMA results in ordinary VGPRs: the scan feeds them to VALU work
+           # every step, and accumulator-register copies would serialise it
+           "-mllvm", "-amdgpu-mfma-vgpr-form",
            "-Wall", "-I", INCLUDE, "-I", CSRC, "-o", tmp]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]
     if verbose:

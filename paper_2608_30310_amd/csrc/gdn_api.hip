@@ -33,6 +33,8 @@ namespace {
 thread_local std::string t_last_error;
 
 constexpr int kThreads = 256;
+// grid limits in make_plan assume <= 256 threads and <= 4 scan workgroups per (sequence, head)
+static_assert(kThreads <= 256 && kScanThreads <= 256 && 128 / kScanCols <= 4, "grid limits");
 
 // ------------------------------------------------------------ host side
 gdn_status fail(gdn_status st, const std::string& msg) {
@@ -104,9 +106,9 @@ gdn_status run(const Args& a) {
   }
   if ((st = mark(a, 1)) != GDN_OK) return st;
   const uint32_t units = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kScanCols);
-  hipLaunchKernelGGL((k_scan<TIn, DK, FWD>), dim3(units), dim3(kScanWaves * kWave), 0, a.stream,
-                     a.cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v), Kw,
-                     Tw, Sw, Pw, a.state_in, static_cast<TIn*>(a.o), a.state_out);
+  hipLaunchKernelGGL((k_scan<TIn, DK, FWD>), dim3(units), dim3(kScanThreads), 0, a.stream,
+                     a.cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v), Kw, Tw, Sw, Pw,
+                     a.state_in, static_cast<TIn*>(a.o), a.state_out);
   if ((st = check_launch("scan launch")) != GDN_OK) return st;
   return mark(a, 2);
 }

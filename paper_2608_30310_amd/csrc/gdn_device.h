@@ -41,15 +41,24 @@ struct Frag {
 
 // Split of eight values with the hardware bf16 conversion: hi = bf16(x),
 // lo = bf16(x - hi).  The conversion's rounding only moves weight between hi
-// and lo; the pair still carries x to ~2^-16 relative.
+// and lo; the pair still carries x to ~2^-16 relative.  Per pair of values:
+// one packed conversion for hi, the two hi values back as fp32 by a shift and
+// a mask of the packed word, two subtractions, one packed conversion for lo.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ Frag split8(const float (&v)[8]) {
-  f32x8 x;
+  u32x4 hi, lo;
 #pragma unroll
-  for (int j = 0; j < 8; ++j) x[j] = v[j];
+  for (int p = 0; p < 4; ++p) {
+    const f32x2 x = {v[2 * p], v[2 * p + 1]};
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2));
+    const f32x2 d = {x[0] - __uint_as_float(h << 16), x[1] - __uint_as_float(h & 0xFFFF0000u)};
+    hi[p] = h;
+    lo[p] = __builtin_bit_cast(uint32_t, __builtin_convertvector(d, bf16x2));
+  }
   Frag f;
-  f.hi = __builtin_convertvector(x, bf16x8);
-  const f32x8 back = __builtin_convertvector(f.hi, f32x8);
-  f.lo = __builtin_convertvector(x - back, bf16x8);
+  f.hi = __builtin_bit_cast(bf16x8, hi);
+  f.lo = __builtin_bit_cast(bf16x8, lo);
   return f;
 }
 

@@ -13,8 +13,9 @@
 //
 // Everything is written to the workspace as ready-made MFMA A operands in the
 // order the scan consumes them (k slots permuted by kperm): T and P split into
-// bf16 hi/lo (only their six nonzero fragments), the per-row scalars, and, by
-// the first value head of each key head, the K record (K, K^T and Q operands).
+// bf16 hi/lo (only their six nonzero fragments), the per-row scalars and, by
+// the first value head of each key head, the K record (K, K^T and Q as
+// operands; split into hi/lo for fp32 inputs).
 #pragma once
 
 #include "gdn_device.h"
@@ -175,7 +176,8 @@ __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, i
 #pragma unroll
     for (int i = 0; i < 16; ++i) Ts[16 * b + i][16 * b + jj] = x[i];
   } else if (h % grp == 0) {
-    // ---- meanwhile, the K record of this key head: K, K^T (and Q) as A operands.
+    // ---- meanwhile, the K record of this key head: K, K^T (and Q) as bf16 A
+    //      operands (hi and lo parts for fp32 inputs).
     //      fragment f, lane (g, r), element j:
     //        K   (ti, kk): K[16 ti + r][32 kk + kperm(g, j)]            f = ti * NK + kk
     //        K^T (td, kk): K[32 kk + kperm(g, j)][16 td + r]            f = NKA + 2 td + kk

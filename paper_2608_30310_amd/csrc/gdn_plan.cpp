@@ -55,12 +55,15 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
     *err = "too many chunks";
     return GDN_ERR_UNSUPPORTED;
   }
-  if (static_cast<int64_t>(N) * hv * 4 > std::numeric_limits<int32_t>::max()) {
+  // A grid dimension counts at most 2^32 - 1 work items; every kernel uses at
+  // most 256 threads per workgroup and at most 4 workgroups per (sequence, head).
+  constexpr int64_t kMaxGroups = std::numeric_limits<uint32_t>::max() / 256;
+  if (static_cast<int64_t>(N) * hv * 4 > kMaxGroups) {
     *err = "num_seqs * num_v_heads too large";
     return GDN_ERR_UNSUPPORTED;
   }
 
-  if (slots > std::numeric_limits<int32_t>::max() / 2) {
+  if (slots > kMaxGroups) {
     *err = "too many chunk slots";
     return GDN_ERR_UNSUPPORTED;
   }

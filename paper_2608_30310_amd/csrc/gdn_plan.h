@@ -19,11 +19,12 @@ constexpr size_t kAlign = 256;    // alignment of every workspace region
 inline int64_t chunk_slot(int64_t seq_start, int64_t seq) { return seq_start / kChunk + seq; }
 
 // Workspace records.  A fragment is one MFMA operand for a whole wave: 64 lanes
-// x 8 bf16 = 1 KiB.  Per (slot, key head), the K record holds the chunk's keys
-// as A operands for K M (4 row tiles x d_k/32 k steps), for K^T Delta
-// (d_k/16 row tiles x 2 k steps) and, with outputs, the queries for Q M; fp32
-// inputs store a high and a low bf16 part.  Per (slot, value head), T and P
-// keep their six nonzero fragments (hi + lo) and S the per-row scalars.
+// x 8 bf16 = 1 KiB.  Per (slot, value head), T and P keep their six nonzero
+// fragments (hi + lo) and S the per-row scalars.  Per (slot, key head), the K
+// record holds the chunk's keys as A operands for K M (4 row tiles x d_k/32 k
+// steps) and for K^T Delta (d_k/16 row tiles x 2 k steps) and, with outputs,
+// the queries for Q M: one bf16 part for bf16 inputs (exact), hi and lo parts
+// for fp32 inputs.
 constexpr size_t kFragBytes = 1024;
 constexpr int kTFrags = 6;                                   // nonzero (row tile, k step) pairs
 constexpr size_t kTRecordBytes = 2 * kTFrags * kFragBytes;   // T, split hi/lo

@@ -85,12 +85,23 @@ def test_workspace_size_null_args():
 
 
 def test_workspace_size_values():
-    # 13 chunks of 64 for 819 tokens; T matrices 13*32*64*64*4 bytes dominate
+    # 819 tokens -> 13 chunk slots.  Per (slot, value head): T as 6 split
+    # fragments (12 KiB) + 5 rows of 64 fp32 scalars; outputs add P (12 KiB).
+    # Per (slot, key head): the K record, (K, K^T [, Q]) = (16 + 16 [+ 16]) 1 KiB
+    # fragments for d_k = 128, one bf16 part for bf16 inputs, hi and lo for fp32.
+    t_rec, s_rec, frag = 6 * 2 * 1024, 5 * 64 * 4, 1024
     st, n = _ws_size(_shape(), _cu([0, 819]))
     assert st == 0
-    assert n >= 13 * 32 * 64 * 64 * 4
+    assert n == 13 * 32 * (t_rec + s_rec) + 13 * 16 * 32 * frag
     st, nf = _ws_size(_shape(), _cu([0, 819]), 1)
-    assert st == 0 and nf >= n + 13 * 32 * 64 * 64 * 4
+    assert st == 0 and nf == n + 13 * 32 * t_rec + 13 * 16 * 16 * frag
+    st, n32 = _ws_size(_shape(qkv_dtype=binding.GDN_F32), _cu([0, 819]))
+    assert st == 0 and n32 == n + 13 * 16 * 32 * frag
+    st, n64 = _ws_size(_shape(d_k=64), _cu([0, 819]))
+    assert st == 0 and n64 == 13 * 32 * (t_rec + s_rec) + 13 * 16 * 16 * frag
+    # two sequences: slots cu[n]/64 + n + j, the last ends at 100/64 + 1 + 1 = 3
+    st, n2 = _ws_size(_shape(num_seqs=2), _cu([0, 100, 130]))
+    assert st == 0 and n2 == 3 * 32 * (t_rec + s_rec) + 3 * 16 * 32 * frag
     st, z = _ws_size(_shape(num_seqs=0), _cu([0]))
     assert st == 0 and z < 1024
     assert gdn.workspace_size(1, 16, 32, 128, 128, [0, 819]) == n
