@@ -11,13 +11,22 @@ Default workload: one GDN layer with hybrid-model head shapes (16 key heads,
 prefix 8192 tokens, replay tail 819 tokens (10 %), 512 suffix tokens.
 
 Prints ONE JSON line.  ``value`` is tokens through the path per second
-(tail + suffix tokens per step / step time).  Per-stage durations come from
-HIP events that the library records between its kernels on the stream the
-kernels run on; ``roofline`` describes the dominant kernel.
+(tail + suffix tokens per step / step time), launched eagerly on one stream
+(``ms_per_step_graph`` gives the same step replayed from a HIP graph).  Per-stage
+kernel durations come from HIP events that the library records between its
+kernels on the stream the kernels run on, in a separate pass of the same
+steps; ``roofline`` describes the dominant kernel.
+
+``--summarize-pmc FETCH_DIR WRITE_DIR`` (no GPU) turns two rocprofv3 --pmc
+runs of ``bench.py --calib-copy`` (FETCH_SIZE, then WRITE_SIZE) into the
+traffic summary under profiles/ that later runs report as ``traffic``.
 """
 from __future__ import annotations
 
 import argparse
+import csv
+import glob
+import hashlib
 import json
 import os
 import platform
@@ -25,10 +34,18 @@ import statistics
 import sys
 import time
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
 METRIC = "GDN tail-replay tokens/sec/GPU + state-rebuild latency; % of MFMA roofline"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 CHUNK = 64
+CALIB_BYTES = 256 << 20        # plain copy used to calibrate the PMC byte counters
+FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload1_r{r}.json")
+KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
+                  "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
+                  "paper_2608_30310_amd/csrc/gdn_intra.h", "paper_2608_30310_amd/csrc/gdn_scan.h",
+                  "paper_2608_30310_amd/csrc/gdn_api.hip", "paper_2608_30310_amd/build.py")
 
 
 def parse():
@@ -41,7 +58,21 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="approximate CPU time for the oracle baseline sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
+    ap.add_argument("--cold-reps", type=int, default=20,
+                    help="tail replays timed after an Infinity Cache flush")
+    ap.add_argument("--calib-copy", action="store_true",
+                    help="also run plain device copies of a known size (PMC calibration)")
+    ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
     return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(rel.encode() + b"\0" + f.read())
+    return h.hexdigest()
 
 
 def per_token_work(hk, hv, dk, dv, elt, outputs):
@@ -60,8 +91,96 @@ def per_token_work(hk, hv, dk, dv, elt, outputs):
     return flops, nbytes
 
 
+def quantiles(xs):
+    xs = sorted(xs)
+    pick = lambda q: xs[min(len(xs) - 1, int(round(q * (len(xs) - 1))))]
+    return {"p10": pick(0.1), "p50": statistics.median(xs), "p90": pick(0.9)}
+
+
+# ---------------------------------------------------------------- PMC summary
+def _counter_rows(d):
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no *counter_collection.csv under {d}")
+    rows = []
+    for fn in files:
+        with open(fn) as f:
+            rows += list(csv.DictReader(f))
+    return rows
+
+
+def _per_kernel_mean(rows, counter):
+    """Mean over dispatches of the counter, per kernel name (KiB per dispatch)."""
+    per = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        key = (r["Kernel_Name"], r.get("Dispatch_Id") or r.get("Correlation_Id"))
+        per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
+    out = {}
+    for (name, _), v in per.items():
+        out.setdefault(name, []).append(v)
+    return {name: statistics.fmean(v) for name, v in out.items()}
+
+
+def summarize_pmc(fetch_dir, write_dir, replay):
+    fetch = _per_kernel_mean(_counter_rows(fetch_dir), "FETCH_SIZE")
+    write = _per_kernel_mean(_counter_rows(write_dir), "WRITE_SIZE")
+    copy = [n for n in fetch if "neg" in n and "gdn" not in n]
+    if not copy:
+        raise SystemExit("no calibration kernel in the FETCH_SIZE run: rerun bench.py with --calib-copy")
+    # the calibration kernel reads and writes CALIB_BYTES
+    cname = max(copy, key=lambda n: fetch[n])
+    f_fetch = CALIB_BYTES / (fetch[cname] * 1024.0)
+    f_write = CALIB_BYTES / (write[cname] * 1024.0)
+    kernels = {}
+    for name in fetch:
+        if "k_scan" not in name and "k_intra" not in name:
+            continue
+        short = name.split("(")[0].replace("void ", "")
+        fb = fetch[name] * 1024.0 * f_fetch
+        wb = write.get(name, 0.0) * 1024.0 * f_write
+        kernels[short] = {"fetch_kib": fetch[name], "write_kib": write.get(name, 0.0),
+                          "fetch_bytes": fb, "write_bytes": wb, "traffic_bytes": fb + wb}
+    summary = {"workload": f"one layer Hk=16 Hv=32 d=128 bf16, tail {replay} + suffix 512",
+               "source_sha256": kernel_source_hash(),
+               "calibration": {"kernel": cname.split("(")[0], "bytes_each_way": CALIB_BYTES,
+                               "fetch_kib": fetch[cname], "write_kib": write[cname],
+                               "fetch_factor": f_fetch, "write_factor": f_write},
+               "kernels": kernels,
+               "commands": [
+                   "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE "
+                   "--output-format csv -d $ROOT/gpurun_out/pmc_fetch -o fetch -- python3 $ROOT/bench.py "
+                   "--no-cpu-baseline --no-graph --steps 5 --warmup 2 --cold-reps 0 --calib-copy",
+                   "(same with WRITE_SIZE into $ROOT/gpurun_out/pmc_write)",
+                   f"python bench.py --summarize-pmc gpurun_out/pmc_fetch gpurun_out/pmc_write"]}
+    path = TRAFFIC_FILE.format(r=replay)
+    with open(path, "w") as f:
+        json.dump(summary, f, indent=1)
+    print(json.dumps(summary, indent=1))
+    return path
+
+
+def load_traffic(replay, kernel_short):
+    """Calibrated HBM bytes per launch of `kernel_short` from the committed PMC
+    summary, or None when there is none or the kernels changed since."""
+    path = TRAFFIC_FILE.format(r=replay)
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        s = json.load(f)
+    if s.get("source_sha256") != kernel_source_hash():
+        return None
+    k = s["kernels"].get(kernel_short)
+    return None if k is None else k["traffic_bytes"]
+
+
+# ---------------------------------------------------------------- main
 def main():
     args = parse()
+    if args.summarize_pmc:
+        summarize_pmc(*args.summarize_pmc, args.replay)
+        return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(the per-(sequence, head) work shards with no exchange; see DESIGN.md)",
@@ -114,37 +233,98 @@ def main():
             e.record()
         return evs
 
-    def step(ev_t=None, ev_f=None):
+    def replay_call(ev=None):
         gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"],
-                        state_out=state, workspace=ws_t, events=ev_t)
+                        state_out=state, workspace=ws_t, events=ev)
+
+    def forward_call(ev=None):
         gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
-                          state_in=state, o=o, state_out=state2, workspace=ws_f, events=ev_f)
+                          state_in=state, o=o, state_out=state2, workspace=ws_f, events=ev)
+
+    def step(ev_t=None, ev_f=None):
+        replay_call(ev_t)
+        forward_call(ev_f)
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-
     K = args.steps
+
+    def timed(fn):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(K):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / K
+
+    # ---- graph of one step, checked bitwise against the eager step on several replays
+    graph, graph_note = None, None
+    if not args.no_graph:
+        step()
+        torch.cuda.synchronize()
+        want_s, want_o = state2.clone(), o.clone()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        ok = True
+        for _ in range(3):
+            state2.zero_()
+            o.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            ok = ok and torch.equal(state2, want_s) and torch.equal(o, want_o)
+            step()               # eager work between replays
+            torch.cuda.synchronize()
+        if ok:
+            graph = g
+        else:
+            graph_note = "graph replay differed from the eager step; timed eagerly"
+
+    ms_per_step = timed(step)
+    ms_graph = timed(graph.replay) if graph is not None else None
+
+    # ---- per-stage kernel durations: events recorded by the library on its stream
     ev_t = [new_events(len(names_t) + 1) for _ in range(K)]
     ev_f = [new_events(len(names_f) + 1) for _ in range(K)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    start.record()
     for i in range(K):
         step(ev_t[i], ev_f[i])
-    stop.record()
     torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    ms_per_step = total_ms / K
-
     stages = {}
     for prefix, names, evs in (("tail_replay", names_t, ev_t), ("chunk_forward", names_f, ev_f)):
         for j, nm in enumerate(names):
             d = [evs[i][j].elapsed_time(evs[i][j + 1]) * 1e3 for i in range(K)]
             stages[f"{prefix}.{nm}"] = {"mean_us": statistics.fmean(d),
                                         "median_us": statistics.median(d)}
-    rebuild = [ev_t[i][0].elapsed_time(ev_t[i][-1]) * 1e3 for i in range(K)]
-    rebuild_us = statistics.median(rebuild)
+    warm = quantiles([ev_t[i][0].elapsed_time(ev_t[i][-1]) * 1e3 for i in range(K)])
+
+    # ---- cold rebuild latency: Infinity Cache flushed before each tail replay
+    cold = None
+    if args.cold_reps > 0:
+        flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
+        lat = []
+        for i in range(args.cold_reps):
+            flush.fill_(float(i))
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            replay_call()
+            b.record()
+            torch.cuda.synchronize()
+            lat.append(a.elapsed_time(b) * 1e3)
+        cold = quantiles(lat)
+        del flush
+
+    if args.calib_copy:
+        # a plain elementwise kernel that reads and writes CALIB_BYTES once each
+        src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
 
     # ---- algorithmic work
     elt = 2
@@ -158,15 +338,23 @@ def main():
     t_s = ms_per_step * 1e-3
     path_bound_s = max(path_flops / (BF16_PEAK_TFLOPS * 1e12), path_bytes / (HBM_PEAK_GBS * 1e9))
 
-    # dominant kernel: the stage with the largest mean time per step
+    # dominant kernel: the stage with the largest mean time per step; its
+    # algorithmic bytes are those of the call it belongs to
     dom = max(stages, key=lambda k: stages[k]["mean_us"])
     dom_call = dom.split(".")[0]
     kbytes = tail_bytes if dom_call == "tail_replay" else fwd_bytes
+    kflops = tail_flops if dom_call == "tail_replay" else fwd_flops
     dom_s = stages[dom]["mean_us"] * 1e-6
     achieved = kbytes / dom_s / 1e9
+    kname = {"tail_replay.scan": "gdn::k_scan<unsigned short, 128, false>",
+             "chunk_forward.scan": "gdn::k_scan<unsigned short, 128, true>",
+             "tail_replay.intra": "gdn::k_intra<unsigned short, 128, false>",
+             "chunk_forward.intra": "gdn::k_intra<unsigned short, 128, true>"}.get(dom)
+    traffic = load_traffic(args.replay, kname) if kname else None
     roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
-                "algorithmic_bytes_per_launch": kbytes}
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
+                "algorithmic_bytes_per_launch": kbytes,
+                "mfma_frac": kflops / dom_s / (BF16_PEAK_TFLOPS * 1e12)}
 
     tokens = r + s
     result = {
@@ -186,8 +374,12 @@ def main():
                                f"prefix 8192, tail replay r={r} from zero + {s}-token suffix "
                                f"forward with outputs",
                    "global_batch": 1, "seq_len": r + s, "parallelism": "single GPU"},
-        "rebuild_latency_us": rebuild_us,
-        "replay_tokens_per_s": r / (rebuild_us * 1e-6),
+        "launch": "eager",
+        "ms_per_step_graph": ms_graph,
+        "rebuild_latency_us": warm["p50"],
+        "rebuild_latency_warm_us": warm,
+        "rebuild_latency_cold_us": cold,
+        "replay_tokens_per_s": r / (warm["p50"] * 1e-6),
         "stages": stages,
         "path": {"flops": path_flops, "bytes": path_bytes, "roofline_us": path_bound_s * 1e6,
                  "roofline_frac": path_bound_s / t_s,
@@ -196,6 +388,8 @@ def main():
         "cpu_baseline": None,
         "gpu": torch.cuda.get_device_name(dev),
     }
+    if graph_note:
+        result["note"] = graph_note
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(tail, suf, r, s, args.cpu_seconds)

@@ -16,6 +16,19 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWave = 64;
 
+// The command processor hands workgroups to the 8 XCDs round-robin by linear
+// index (workgroup b runs on XCD b % 8), and each XCD has its own L2.  The map
+// below turns b into a logical index such that every XCD receives one
+// contiguous range of logical indices, so workgroups that are logically
+// adjacent (and read the same records) share an L2.  It is a bijection on
+// [0, total) whatever the hardware order, so correctness never depends on it.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_remap(int b, int total) {
+  const int x = b % kXcds, i = b / kXcds;
+  const int per = total / kXcds, rem = total % kXcds;
+  return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
+}
+
 // ---------------------------------------------------------------- bf16
 __device__ __forceinline__ uint16_t f2bf(float x) {
   // round to nearest, ties to even (finite values)

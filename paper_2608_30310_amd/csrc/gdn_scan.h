@@ -141,9 +141,12 @@ void k_scan(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
   const int lane = tid % kWave;
   const int lg = lane / 16, lr = lane % 16;
   const int ngroups = dv / kScanCols;
-  const int cgrp = blockIdx.x % ngroups;
-  const int h = (blockIdx.x / ngroups) % hv;
-  const int n = blockIdx.x / (ngroups * hv);
+  // logical unit: the column groups of a value head, then the value heads of a
+  // key head, are adjacent (same XCD, shared records in its L2)
+  const int unit = xcd_remap(blockIdx.x, gridDim.x);
+  const int cgrp = unit % ngroups;
+  const int h = (unit / ngroups) % hv;
+  const int n = unit / (ngroups * hv);
   const int kh = h / (hv / hk);
   const int col0 = kScanCols * cgrp;           // first state column of the workgroup
   const int wcol = 16 * wave + lr;             // this lane's column within the workgroup
