@@ -75,6 +75,16 @@ __device__ __forceinline__ Frag split8(const float (&v)[8]) {
   return f;
 }
 
+// Transposing LDS read (ds_read_b64_tr_b16): within each group of 16 lanes,
+// the lanes' 8-byte rows X[lane][0..3] form a 16 x 4 matrix of 16-bit values
+// and lane i receives X[i/4 + 4j][i%4], j = 0..3.
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4* lds_s16x4_ptr_t;
+__device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
+  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr_t)p);
+  return __builtin_bit_cast(u32x2, v);
+}
+
 // Reinterpret two 8-byte halves (4 bf16 each) as one operand.
 __device__ __forceinline__ bf16x8 join_halves(u32x2 a, u32x2 b) {
   u32x4 u = u32x4{a.x, a.y, b.x, b.y};

@@ -6,10 +6,11 @@
 //   T    = (I + A)^-1                          unit lower triangular
 //   P_ij = scale e^{G_i - G_j} (q_i . k_j)     for j <= i, else 0   (outputs only)
 // K K^T and Q K^T run on MFMA (bf16 inputs are exact operands; fp32 inputs are
-// split hi/lo).  T is formed in fp32 by blocked forward substitution: the four
-// diagonal 16x16 blocks by column substitution in registers, then each column
-// block b on its own wave, T_ab = -T_aa (sum_{m=b}^{a-1} A_am T_mb) for
-// a = b+1..3, with fp32 MFMA (exact fp32 products).
+// split hi/lo).  T is formed in fp32: the four diagonal 16x16 blocks by forward
+// substitution in registers, then the off-diagonal blocks from the inverse of a
+// 2x2 lower block triangular matrix (lower-left block -T22 A21 T11), applied to
+// 16-row blocks and then to the 32-row halves, with fp32 MFMA (exact fp32
+// products).
 //
 // Everything is written to the workspace as ready-made MFMA A operands in the
 // order the scan consumes them (k slots permuted by kperm): T and P split into
@@ -78,8 +79,9 @@ __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, i
   __shared__ __attribute__((aligned(16))) float As[kChunk][AP];   // A (strictly lower)
   __shared__ __attribute__((aligned(16))) float Ts[kChunk][AP];   // T = (I + A)^-1
   __shared__ __attribute__((aligned(16))) float Ps[FWD ? kChunk : 1][AP];
-  __shared__ __attribute__((aligned(16))) float Ys[3][16][17];    // per-wave block scratch
-  __shared__ float Gs[kChunk], Bs[kChunk];
+  __shared__ __attribute__((aligned(16))) float Ys[4][16][17];    // per-wave block scratch
+  __shared__ __attribute__((aligned(16))) float Gs[kChunk];
+  __shared__ __attribute__((aligned(16))) float Bs[kChunk];
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
@@ -122,57 +124,97 @@ __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, i
   }
   __syncthreads();
 
-  // ---- K K^T (and Q K^T) on MFMA, 10 lower tiles over 4 waves, turned into A (and P)
-  for (int t = wave; t < 10; t += 4) {
-    const int bi = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
-    const int bj = t - bi * (bi + 1) / 2;
-    f32x4 acc = zero4(), accq = zero4();
+  // ---- K K^T (and Q K^T) on MFMA, 10 lower tiles over 4 waves (tiles wave,
+  //      wave + 4, wave + 8), turned into A (and P).  All operand reads first,
+  //      then the MFMAs, then the elementwise pass.
+  {
+    constexpr int TPW = 3;   // tiles per wave, at most
+    Frag fa[TPW][NK], fb[TPW][NK], fq[TPW][NK];
+    f32x4 acc[TPW], accq[TPW];
+    auto tile_rc = [](int t, int& bi, int& bj) __attribute__((always_inline)) {
+      bi = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
+      bj = t - bi * (bi + 1) / 2;
+    };
 #pragma unroll
-    for (int kk = 0; kk < NK; ++kk) {
-      const int c = 32 * kk + 8 * lg;
-      Frag a, b;
-      a.hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bi + lr][c]);
-      b.hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bj + lr][c]);
-      if constexpr (SPLIT) {
-        a.lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bi + lr][c]);
-        b.lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bj + lr][c]);
-        acc = mma_x3(a, b, acc);
-      } else {
-        acc = mma(a.hi, b.hi, acc);
-      }
-      if constexpr (FWD) {
-        Frag qa;
-        qa.hi = *reinterpret_cast<const bf16x8*>(&Qs[0][16 * bi + lr][c]);
-        if constexpr (SPLIT) {
-          qa.lo = *reinterpret_cast<const bf16x8*>(&Qs[NL - 1][16 * bi + lr][c]);
-          accq = mma_x3(qa, b, accq);
-        } else {
-          accq = mma(qa.hi, b.hi, accq);
+    for (int u = 0; u < TPW; ++u) {
+      const int t = wave + 4 * u;
+      if (t < 10) {
+        int bi, bj;
+        tile_rc(t, bi, bj);
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+          const int c = 32 * kk + 8 * lg;
+          fa[u][kk].hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bi + lr][c]);
+          fb[u][kk].hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bj + lr][c]);
+          if constexpr (SPLIT) {
+            fa[u][kk].lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bi + lr][c]);
+            fb[u][kk].lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bj + lr][c]);
+          }
+          if constexpr (FWD) {
+            fq[u][kk].hi = *reinterpret_cast<const bf16x8*>(&Qs[0][16 * bi + lr][c]);
+            if constexpr (SPLIT) fq[u][kk].lo = *reinterpret_cast<const bf16x8*>(&Qs[NL - 1][16 * bi + lr][c]);
+          }
         }
       }
     }
-    const int j = 16 * bj + lr;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int i = 16 * bi + 4 * lg + r;
-      const float decay = j <= i ? __expf(Gs[i] - Gs[j]) : 0.f;
-      As[i][j] = j < i ? Bs[i] * decay * acc[r] : 0.f;
-      if constexpr (FWD) Ps[i][j] = scale * decay * accq[r];
+    for (int u = 0; u < TPW; ++u) {
+      acc[u] = zero4();
+      accq[u] = zero4();
+      if (wave + 4 * u < 10) {
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+          if constexpr (SPLIT) {
+            acc[u] = mma_x3(fa[u][kk], fb[u][kk], acc[u]);
+            if constexpr (FWD) accq[u] = mma_x3(fq[u][kk], fb[u][kk], accq[u]);
+          } else {
+            acc[u] = mma(fa[u][kk].hi, fb[u][kk].hi, acc[u]);
+            if constexpr (FWD) accq[u] = mma(fq[u][kk].hi, fb[u][kk].hi, accq[u]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+      const int t = wave + 4 * u;
+      if (t < 10) {
+        int bi, bj;
+        tile_rc(t, bi, bj);
+        const int j = 16 * bj + lr;
+        const float gj = Gs[j];
+        const f32x4 gi = *reinterpret_cast<const f32x4*>(&Gs[16 * bi + 4 * lg]);
+        const f32x4 bi4 = *reinterpret_cast<const f32x4*>(&Bs[16 * bi + 4 * lg]);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int i = 16 * bi + 4 * lg + r;
+          const float decay = j <= i ? __expf(gi[r] - gj) : 0.f;
+          As[i][j] = j < i ? bi4[r] * decay * acc[u][r] : 0.f;
+          if constexpr (FWD) Ps[i][j] = scale * decay * accq[u][r];
+        }
+      }
     }
   }
   __syncthreads();
 
   if (wave == 0) {
-    // ---- diagonal 16x16 blocks of T: lane = (block, column), column substitution
+    // ---- diagonal 16x16 blocks of T: lane = (block b, column j).  The block's
+    //      rows are read once as 16-byte pieces; forward substitution runs
+    //      right-looking (row i takes A_im x_m as soon as x_m is final), so every
+    //      step has independent FMAs.
     const int b = lane >> 4, jj = lane & 15;
+    f32x4 arow[16][4];
+#pragma unroll
+    for (int i = 1; i < 16; ++i)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (4 * c < i) arow[i][c] = *reinterpret_cast<const f32x4*>(&As[16 * b + i][16 * b + 4 * c]);
     float x[16];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      float s = (i == jj) ? 1.f : 0.f;
+    for (int i = 0; i < 16; ++i) x[i] = (i == jj) ? 1.f : 0.f;
 #pragma unroll
-      for (int m = 0; m < i; ++m) s -= As[16 * b + i][16 * b + m] * x[m];
-      x[i] = s;
-    }
+    for (int m = 0; m < 15; ++m)
+#pragma unroll
+      for (int i = m + 1; i < 16; ++i) x[i] -= arow[i][m / 4][m % 4] * x[m];
 #pragma unroll
     for (int i = 0; i < 16; ++i) Ts[16 * b + i][16 * b + jj] = x[i];
   } else if (h % grp == 0) {
@@ -184,53 +226,106 @@ __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, i
     //        Q   (ti, kk): Q[16 ti + r][32 kk + kperm(g, j)]            f = NKA + NKT + ti * NK + kk
     //      record layout [hi | lo][fragment][lane]
     u32x4* kdst = Kw + (static_cast<int64_t>(slot) * hk + kh) * (NL * NKF * kWave);
-    for (int e = tid - kWave; e < NL * NKF * kWave; e += 256 - kWave) {
-      const int p = e / (NKF * kWave), f = (e / kWave) % NKF, fl = e % kWave;
-      const int fg = fl / 16, fr = fl % 16;
-      u32x4 val;
-      if (f < NKA) {
-        const int ti = f / NK, kk = f % NK;
-        val = __builtin_bit_cast(u32x4, perm_frag(&Ks[p][16 * ti + fr][32 * kk + 4 * fg]));
-      } else if (f < NKA + NKT) {
-        const int td = (f - NKA) / 2, kk = (f - NKA) % 2;
-        uint16_t v8[8];
+    // Three waves share each kind of fragment; every wave first reads all of its
+    // fragments (indices clamped so the reads are unconditional), then stores.
+    auto ka_val = [&](int p, int f) __attribute__((always_inline)) {   // f < NKA
+      const int ti = f / NK, kk = f % NK;
+      return __builtin_bit_cast(u32x4, perm_frag(&Ks[p][16 * ti + lr][32 * kk + 4 * lg]));
+    };
+    auto kt_val = [&](int p, int f) __attribute__((always_inline)) {   // f < NKT
+      // two transposing reads: lane (g, r) of each 16-lane group addresses row
+      // 32 kk + 4 g + r / 4 (then 16 rows further), columns 16 td + 4 (r % 4)..+3,
+      // and receives rows 32 kk + kperm(g, j) of column 16 td + r
+      const int td = f / 2, kk = f % 2;
+      const int row = 32 * kk + 4 * lg + lr / 4, c = 16 * td + 4 * (lr % 4);
+      return __builtin_bit_cast(u32x4, join_halves(lds_read_tr16(&Ks[p][row][c]),
+                                                   lds_read_tr16(&Ks[p][row + 16][c])));
+    };
+    auto q_val = [&](int p, int f) __attribute__((always_inline)) {    // f < NKA
+      const int ti = f / NK, kk = f % NK;
+      return __builtin_bit_cast(
+          u32x4, perm_frag(&Qs[FWD ? p : 0][FWD ? 16 * ti + lr : 0][FWD ? 32 * kk + 4 * lg : 0]));
+    };
+    constexpr int PA = (NKA + 2) / 3, PT = (NKT + 2) / 3;   // per wave, per part
+    const int w3 = wave - 1;                                 // 0..2
 #pragma unroll
-        for (int j = 0; j < 8; ++j) v8[j] = Ks[p][32 * kk + kperm(fg, j)][16 * td + fr];
-        val = u32x4{v8[0] | (uint32_t(v8[1]) << 16), v8[2] | (uint32_t(v8[3]) << 16),
-                    v8[4] | (uint32_t(v8[5]) << 16), v8[6] | (uint32_t(v8[7]) << 16)};
-      } else {
-        const int fq = f - NKA - NKT;
-        const int ti = fq / NK, kk = fq % NK;
-        val = __builtin_bit_cast(
-            u32x4, perm_frag(&Qs[FWD ? p : 0][FWD ? 16 * ti + fr : 0][FWD ? 32 * kk + 4 * fg : 0]));
+    for (int p = 0; p < NL; ++p) {
+      u32x4* pdst = kdst + static_cast<int64_t>(p) * NKF * kWave;
+      u32x4 va[PA], vt[PT], vq[FWD ? PA : 1];
+#pragma unroll
+      for (int i = 0; i < PA; ++i) {
+        va[i] = ka_val(p, min(w3 + 3 * i, NKA - 1));
+        if constexpr (FWD) vq[i] = q_val(p, min(w3 + 3 * i, NKA - 1));
       }
-      kdst[e] = val;
+#pragma unroll
+      for (int i = 0; i < PT; ++i) vt[i] = kt_val(p, min(w3 + 3 * i, NKT - 1));
+#pragma unroll
+      for (int i = 0; i < PA; ++i) {
+        const int f = w3 + 3 * i;
+        if (f < NKA) {
+          pdst[f * kWave + lane] = va[i];
+          if constexpr (FWD) pdst[(NKA + NKT + f) * kWave + lane] = vq[i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < PT; ++i) {
+        const int f = w3 + 3 * i;
+        if (f < NKT) pdst[(NKA + f) * kWave + lane] = vt[i];
+      }
     }
   }
   __syncthreads();
 
-  // ---- off-diagonal blocks, one column block per wave (fp32 MFMA):
-  //      T_ab = -T_aa (sum_{m=b}^{a-1} A_am T_mb), a = b+1..3
-  if (wave < 3) {
-    const int b = wave;
-    for (int a = b + 1; a < 4; ++a) {
-      f32x4 y = zero4();
-      for (int m = b; m < a; ++m) {
+  // ---- off-diagonal blocks by the block-inverse identity for a lower block
+  //      triangular matrix: inv([[I + A11, 0], [A21, I + A22]]) has lower-left
+  //      block -T22 A21 T11.  First on 16-row blocks (T_10, T_32), then on the
+  //      32-row halves (rows 32..63, columns 0..31).  fp32 MFMA throughout.
+  //      blk_mm: acc += X[xr:xr+16, xc:xc+16] Y[yr:yr+16, yc:yc+16].
+  auto blk_mm = [&](f32x4 acc, const float* X, int xp, const float* Y, int yp) __attribute__((always_inline)) {
+    float xa[4], yb[4];
 #pragma unroll
-        for (int kk = 0; kk < 4; ++kk)
-          y = mma_f32(As[16 * a + lr][16 * m + 4 * kk + lg], Ts[16 * m + 4 * kk + lg][16 * b + lr], y);
-      }
-#pragma unroll
-      for (int r = 0; r < 4; ++r) Ys[b][4 * lg + r][lr] = y[r];
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-      f32x4 x = zero4();
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        x = mma_f32(Ts[16 * a + lr][16 * a + 4 * kk + lg], Ys[b][4 * kk + lg][lr], x);
-#pragma unroll
-      for (int r = 0; r < 4; ++r) Ts[16 * a + 4 * lg + r][16 * b + lr] = -x[r];
-      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    for (int kk = 0; kk < 4; ++kk) {
+      xa[kk] = X[lr * xp + 4 * kk + lg];
+      yb[kk] = Y[(4 * kk + lg) * yp + lr];
     }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) acc = mma_f32(xa[kk], yb[kk], acc);
+    return acc;
+  };
+  auto at = [&](float (*M)[AP], int r, int c) __attribute__((always_inline)) { return &M[16 * r][16 * c]; };
+  constexpr int YP = 17;
+  if (wave < 2) {
+    // T_ab = -T_aa A_ab T_bb for (a, b) = (1, 0) (wave 0) and (3, 2) (wave 1)
+    const int a = 2 * wave + 1, bb = 2 * wave;
+    const f32x4 y = blk_mm(zero4(), at(As, a, bb), AP, at(Ts, bb, bb), AP);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Ys[wave][4 * lg + r][lr] = y[r];
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    const f32x4 xx = blk_mm(zero4(), at(Ts, a, a), AP, &Ys[wave][0][0], YP);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Ts[16 * a + 4 * lg + r][16 * bb + lr] = -xx[r];
+  }
+  __syncthreads();
+  // rows 32..63, columns 0..31: wave w owns block (rr, cc) = (2 + w / 2, w % 2);
+  // first Y = A[32:64, 0:32] T[0:32, 0:32] (T_kc = 0 for k < c) ...
+  const int rr = 2 + wave / 2, cc = wave % 2;
+  {
+    f32x4 y = zero4();
+#pragma unroll
+    for (int k = 0; k < 2; ++k)
+      if (k >= cc) y = blk_mm(y, at(As, rr, k), AP, at(Ts, k, cc), AP);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Ys[wave][4 * lg + r][lr] = y[r];
+  }
+  __syncthreads();
+  // ... then -T[32:64, 32:64] Y (T_rk = 0 for k > r)
+  {
+    f32x4 xx = zero4();
+#pragma unroll
+    for (int k = 2; k < 4; ++k)
+      if (k <= rr) xx = blk_mm(xx, at(Ts, rr, k), AP, &Ys[2 * (k - 2) + cc][0][0], YP);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Ts[16 * rr + 4 * lg + r][16 * cc + lr] = -xx[r];
   }
   __syncthreads();
 

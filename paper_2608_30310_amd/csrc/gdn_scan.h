@@ -30,8 +30,6 @@ namespace gdn {
 constexpr int kLdsBytes = 160 * 1024;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
-typedef short s16x4 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) s16x4* lds_s16x4_ptr_t;
 
 // 16 bytes per lane from `src` (per lane) to LDS `dst + 16 * lane` (dst uniform).
 __device__ __forceinline__ void dma16(const void* src, void* dst) {
@@ -39,13 +37,6 @@ __device__ __forceinline__ void dma16(const void* src, void* dst) {
 }
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
-
-// Transposing LDS read: within each group of 16 lanes, the lanes' 8-byte rows
-// X[lane][0..3] form a 16 x 4 matrix and lane i receives X[i/4 + 4j][i%4].
-__device__ __forceinline__ u32x2 lds_read_tr16(const void* p) {
-  const s16x4 v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_ptr_t)p);
-  return __builtin_bit_cast(u32x2, v);
-}
 
 // Byte offset of byte `byte_in_row` of row `row` in a row tile whose rows hold
 // ROW_BYTES / 16 pieces of 16 bytes, piece p of row R stored at p ^ (R % pieces).
