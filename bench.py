@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run plain device copies of a known size (PMC calibration)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--sweep", action="store_true",
+                    help="time the other workloads instead (one JSON line each): small fp32 layer, "
+                         "36-layer stack, 16 varlen hits, replay-vs-full at 8K/16K/32K")
     return ap.parse_args()
 
 
@@ -180,6 +183,9 @@ def main():
     args = parse()
     if args.summarize_pmc:
         summarize_pmc(*args.summarize_pmc, args.replay)
+        return
+    if args.sweep:
+        sweep(args)
         return
     if args.gpus != 1:
         print("bench.py measures one GPU: this build has no multi-GPU path "
@@ -394,6 +400,157 @@ def main():
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(tail, suf, r, s, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+# ---------------------------------------------------------------- other workloads
+def sweep(args):
+    """Latency of the other workloads; one JSON line each.  Inputs of the small
+    layer and of the varlen hits are the seeded ones the parity tests use; the
+    36-layer stack and the replay-vs-full sweep use device-drawn inputs of the
+    same distributions (timing only: the kernels' time does not depend on the
+    values)."""
+    import numpy as np
+    import torch
+
+    import paper_2608_30310_amd as gdn
+    import synth
+    from synth import workloads
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    gdn.load_library()
+    reps, warm = max(args.steps // 2, 10), 5
+
+    def timed_us(fn):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b) * 1e3)
+        return quantiles(ts)
+
+    def packed_dev(p, shape):
+        if shape.dtype == "bf16":
+            qkv = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        else:
+            qkv = lambda a: torch.from_numpy(a).to(dev)
+        return dict(q=qkv(p.q), k=qkv(p.k), v=qkv(p.v), g=torch.from_numpy(p.g).to(dev),
+                    beta=torch.from_numpy(p.beta).to(dev), cu=torch.from_numpy(p.cu_seqlens).to(dev),
+                    cu_host=torch.from_numpy(p.cu_seqlens.copy()))
+
+    def random_dev(lens, hk, hv, d, gate_scale=0.1, seed=0):
+        """Device-drawn inputs with the workload distributions (timing only)."""
+        gen = torch.Generator(device=dev).manual_seed(seed)
+        T = int(sum(lens))
+        nrm = lambda x: (x / x.norm(dim=-1, keepdim=True)).to(torch.bfloat16)
+        q = nrm(torch.randn(T, hk, d, device=dev, generator=gen))
+        k = nrm(torch.randn(T, hk, d, device=dev, generator=gen))
+        v = torch.randn(T, hv, d, device=dev, generator=gen).to(torch.bfloat16)
+        beta = torch.sigmoid(torch.randn(T, hv, device=dev, generator=gen))
+        g = -torch.nn.functional.softplus(torch.randn(T, hv, device=dev, generator=gen)) * gate_scale
+        cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+        return dict(q=q, k=k, v=v, g=g.contiguous(), beta=beta.contiguous(),
+                    cu=torch.from_numpy(cu).to(dev), cu_host=torch.from_numpy(cu))
+
+    def replay(x, state, ws):
+        gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"], state_out=state,
+                        workspace=ws)
+
+    def forward(x, state_in, o, state_out, ws, write_state=True):
+        gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                          state_in=state_in, o=o, state_out=state_out, workspace=ws,
+                          write_state=write_state)
+
+    def buffers(x, n, hk, hv, d, outputs):
+        cu = x["cu_host"].tolist()
+        ws = torch.empty(gdn.workspace_size(n, hk, hv, d, d, cu, dtype=x["k"].dtype,
+                                            with_outputs=outputs) + 256,
+                         dtype=torch.uint8, device=dev)
+        st = torch.empty((n, hv, d, d), dtype=torch.float32, device=dev)
+        o = torch.empty((cu[-1], hv, d), dtype=x["v"].dtype, device=dev) if outputs else None
+        return ws, st, o
+
+    def emit(rec):
+        print(json.dumps(rec), flush=True)
+
+    # ---- small fp32 layer (Hk = Hv = 4, d = 64): tail 205 + suffix 256
+    shape, hits = workloads.workload0()
+    h = hits[0]
+    xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
+    wst, st, _ = buffers(xt, 1, 4, 4, 64, False)
+    wsf, st2, o = buffers(xs, 1, 4, 4, 64, True)
+    rep = timed_us(lambda: replay(xt, st, wst))
+    both = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    emit({"workload": "small fp32 layer Hk=Hv=4 d=64: tail 205 + suffix 256",
+          "rebuild_latency_us": rep, "step_us": both, "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
+
+    # ---- hybrid-model layer, tail 410 (the default bench line covers 819)
+    shape, hits = workloads.workload1(410)
+    h = hits[0]
+    xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
+    wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
+    wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
+    rep = timed_us(lambda: replay(xt, st, wst))
+    both = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    emit({"workload": "one GDN layer Hk=16 Hv=32 d=128 bf16: tail 410 + suffix 512",
+          "rebuild_latency_us": rep, "step_us": both, "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
+
+    # ---- 36-layer stack, m = 32768, r = 3277: 36 sequential per-layer replays,
+    #      and the batched variant (layers as 36 sequences of one launch)
+    L, r2 = 36, 3277
+    xl = [random_dev([r2], 16, 32, 128, seed=100 + l) for l in range(L)]
+    wsl, stl, _ = buffers(xl[0], 1, 16, 32, 128, False)
+    seq = timed_us(lambda: [replay(x, stl, wsl) for x in xl])
+    xb = random_dev([r2] * L, 16, 32, 128, seed=7)
+    wsb, stb, _ = buffers(xb, L, 16, 32, 128, False)
+    bat = timed_us(lambda: replay(xb, stb, wsb))
+    emit({"workload": "36-layer stack Hk=16 Hv=32 d=128 bf16, m=32768, tail 3277 per layer",
+          "rebuild_latency_sequential_us": seq, "rebuild_latency_batched_us": bat,
+          "replay_tokens_per_s_sequential": L * r2 / (seq["p50"] * 1e-6),
+          "replay_tokens_per_s_batched": L * r2 / (bat["p50"] * 1e-6)})
+
+    # ---- 16 concurrent hits (varlen), one replay launch + one forward launch
+    draw = workloads.workload3_draw()
+    rl = [gdn.replay_len(m, ratio) for m, ratio, _ in draw]
+    shape, hits = workloads.workload3(rl)
+    xt = packed_dev(synth.pack([h.tail(shape) for h in hits]), shape)
+    xs = packed_dev(synth.pack([h.suffix(shape) for h in hits]), shape)
+    n = len(hits)
+    wst, st, _ = buffers(xt, n, 16, 32, 128, False)
+    wsf, st2, o = buffers(xs, n, 16, 32, 128, True)
+    rep = timed_us(lambda: replay(xt, st, wst))
+    both = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    sr, ss = sum(h.r for h in hits), sum(h.s for h in hits)
+    emit({"workload": f"16 varlen hits Hk=16 Hv=32 d=128 bf16: sum r={sr}, sum s={ss}",
+          "rebuild_latency_us": rep, "step_us": both, "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
+          "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
+
+    # ---- replay vs full prefill, suffix 512: t_full = forward(0, m + s) with
+    #      outputs; t_replay = replay(r) + forward(S_m, s); state-only full = replay(m + s)
+    for m in (8192, 16384, 32768):
+        x_full = random_dev([m + 512], 16, 32, 128, seed=m)
+        wsF, stF, oF = buffers(x_full, 1, 16, 32, 128, True)
+        wsR, stR, _ = buffers(x_full, 1, 16, 32, 128, False)
+        t_full = timed_us(lambda: forward(x_full, None, oF, stF, wsF))
+        t_state = timed_us(lambda: replay(x_full, stR, wsR))
+        for pct in ("0.05", "0.1"):
+            # the configs' integers where they round to nearest, else the paper's ceiling
+            r = {(8192, "0.1"): 819, (32768, "0.05"): 1638}.get((m, pct), gdn.replay_len(m, pct))
+            xt = random_dev([r], 16, 32, 128, seed=m + r)
+            xs = random_dev([512], 16, 32, 128, seed=m + 1)
+            wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
+            wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
+            t_rep = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+            emit({"workload": f"replay vs full prefill Hk=16 Hv=32 d=128 bf16, m={m}, r={r}, suffix 512",
+                  "t_full_us": t_full["p50"], "t_full_state_only_us": t_state["p50"],
+                  "t_replay_us": t_rep["p50"], "speedup": t_full["p50"] / t_rep["p50"],
+                  "speedup_state_only_full": t_state["p50"] / t_rep["p50"]})
 
 
 def cpu_baseline(tail, suf, r, s, seconds):
