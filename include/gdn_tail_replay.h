@@ -35,7 +35,7 @@
  *     given (normalising them is the caller's job).
  *   - Zero-length sequences are allowed: tail replay writes a zero state,
  *     forward writes state_in (or zeros when state_in is NULL).
- *   - q, k and v must be 16-byte aligned (GDN_ERR_UNSUPPORTED otherwise); the
+ *   - q, k, v and o must be 16-byte aligned (GDN_ERR_UNSUPPORTED otherwise); the
  *     workspace 256-byte aligned (GDN_ERR_WORKSPACE otherwise).
  *   - Inputs are never written.  state_out may alias state_in only when the two
  *     pointers are equal.  Calls that share a workspace must be ordered on one

@@ -13,8 +13,8 @@
 // Two launches per call, both on the caller's stream:
 //   intra  per (chunk slot, value head), fully parallel: T (and P) as split
 //          bf16 MFMA fragments plus per-row scalars (gdn_intra.h)
-//   scan   per (sequence, value head, 32 state columns), sequential over the
-//          sequence's chunks with the state in registers (gdn_scan.h)
+//   scan   per (sequence, value head), sequential over the sequence's chunks
+//          with the state in registers (gdn_scan.h)
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -33,8 +33,8 @@ namespace {
 thread_local std::string t_last_error;
 
 constexpr int kThreads = 256;
-// grid limits in make_plan assume <= 256 threads and <= 4 scan workgroups per (sequence, head)
-static_assert(kThreads <= 256 && kScanThreads <= 256 && 128 / kScanCols <= 4, "grid limits");
+// grid limits in make_plan assume <= 1024 work items per (sequence, head) in any grid dimension
+static_assert(kThreads <= 256 && kColsThreads <= 256 && head_threads(128) <= 1024, "grid limits");
 
 // ------------------------------------------------------------ host side
 gdn_status fail(gdn_status st, const std::string& msg) {
@@ -85,7 +85,7 @@ gdn_status mark_all(const Args& a) {
   return GDN_OK;
 }
 
-template <typename TIn, int DK, bool FWD>
+template <typename TIn, int DK, int DV, bool FWD>
 gdn_status run(const Args& a) {
   const gdn_shape& s = *a.s;
   const Plan& p = *a.p;
@@ -105,20 +105,38 @@ gdn_status run(const Args& a) {
     if ((st = check_launch("intra launch")) != GDN_OK) return st;
   }
   if ((st = mark(a, 1)) != GDN_OK) return st;
-  const uint32_t units = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kScanCols);
-  hipLaunchKernelGGL((k_scan<TIn, DK, FWD>), dim3(units), dim3(kScanThreads), 0, a.stream,
-                     a.cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v), Kw, Tw, Sw, Pw,
-                     a.state_in, static_cast<TIn*>(a.o), a.state_out);
+  // The column-split kernel has the shortest chunk latency but one workgroup
+  // per CU; use it when its grid fits on the chip at once, else the whole-head
+  // kernel (4x the columns per CU, two waves per SIMD).
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return fail(GDN_ERR_HIP, "querying the device");
+  const uint32_t heads = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads;
+  const uint32_t col_groups = heads * (s.d_v / kColsPerGroup);
+  if (col_groups <= static_cast<uint32_t>(cus)) {
+    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(kColsThreads), 0, a.stream,
+                       a.cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v), Kw, Tw, Sw,
+                       Pw, a.state_in, static_cast<TIn*>(a.o), a.state_out);
+  } else {
+    hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(heads), dim3(head_threads(DV)), 0, a.stream,
+                       a.cu, s.num_k_heads, s.num_v_heads, static_cast<const TIn*>(a.v), Kw, Tw, Sw, Pw,
+                       a.state_in, static_cast<TIn*>(a.o), a.state_out);
+  }
   if ((st = check_launch("scan launch")) != GDN_OK) return st;
   return mark(a, 2);
 }
 
+template <int DK, int DV, bool FWD>
+gdn_status run_dtype(const Args& a) {
+  return a.s->qkv_dtype == GDN_BF16 ? run<uint16_t, DK, DV, FWD>(a) : run<float, DK, DV, FWD>(a);
+}
+
 template <bool FWD>
 gdn_status dispatch(const Args& a) {
-  const bool bf16 = a.s->qkv_dtype == GDN_BF16;
-  if (a.s->d_k == 64)
-    return bf16 ? run<uint16_t, 64, FWD>(a) : run<float, 64, FWD>(a);
-  return bf16 ? run<uint16_t, 128, FWD>(a) : run<float, 128, FWD>(a);
+  const int dk = a.s->d_k, dv = a.s->d_v;
+  if (dk == 64) return dv == 64 ? run_dtype<64, 64, FWD>(a) : run_dtype<64, 128, FWD>(a);
+  return dv == 64 ? run_dtype<128, 64, FWD>(a) : run_dtype<128, 128, FWD>(a);
 }
 
 gdn_status common_checks(const gdn_shape* shape, const int32_t* cu_host, const int32_t* cu,
@@ -200,8 +218,8 @@ gdn_status chunk_forward_impl(const gdn_shape* shape, const int32_t* cu_seqlens_
   if (plan.total_tokens > 0 && (!q || !k || !v || !g || !beta || !o))
     return gdn::fail(GDN_ERR_NULL_ARG, "q, k, v, g, beta and o must be non-NULL");
   if (reinterpret_cast<uintptr_t>(q) % 16 != 0 || reinterpret_cast<uintptr_t>(k) % 16 != 0 ||
-      reinterpret_cast<uintptr_t>(v) % 16 != 0)
-    return gdn::fail(GDN_ERR_UNSUPPORTED, "q, k and v must be 16-byte aligned");
+      reinterpret_cast<uintptr_t>(v) % 16 != 0 || reinterpret_cast<uintptr_t>(o) % 16 != 0)
+    return gdn::fail(GDN_ERR_UNSUPPORTED, "q, k, v and o must be 16-byte aligned");
   if (state_in && state_out && state_in != state_out) {
     const size_t n = static_cast<size_t>(shape->num_seqs) * shape->num_v_heads * shape->d_k *
                      shape->d_v;

@@ -119,6 +119,14 @@ __device__ __forceinline__ f32x4 mma_a(const Frag& a, const Frag& b, f32x4 c) {
   else return mma_x2(a.hi, b, c);
 }
 
+// split A times a B operand that is exact bf16 (SPLIT = false) or split.
+template <bool SPLIT>
+__device__ __forceinline__ f32x4 mma_b(const Frag& a, const Frag& b, f32x4 c) {
+  if constexpr (SPLIT) return mma_x3(a, b, c);
+  c = mma(a.hi, b.hi, c);
+  return mma(a.lo, b.hi, c);
+}
+
 // ---------------------------------------------------------------- k-slot permutation
 // Within a 32-wide k step, MFMA slot 8g + j (g = lane/16, j = 0..7) is mapped to
 // contraction index 4g + j for j < 4 and 16 + 4g + (j - 4) for j >= 4.  With this

@@ -1,9 +1,8 @@
 // Chunk scan kernel: the sequential part of the recurrence.
 //
-// One workgroup per (sequence, value head, 32 state columns): two compute waves
-// each own 16 columns of M = S^T (d_k x d_v) and keep them in registers for the
-// whole sequence, and a third wave only moves data.  Per 64-token chunk, with
-// M0 the state at chunk start:
+// One workgroup per (sequence, value head): d_v/16 waves (two per SIMD for
+// d_v = 128), each owning 16 columns of M = S^T (d_k x d_v) in registers for the
+// whole sequence.  Per 64-token chunk, with M0 the state at chunk start:
 //   R      = diag(beta) V - diag(beta e^G) (K M0)
 //   Delta  = T R                                                  (T from k_intra)
 //   O      = diag(scale e^G) (Q M0) + P Delta                     (outputs only)
@@ -12,13 +11,16 @@
 // step is permuted (kperm) so each accumulator is directly the next product's
 // B operand.  fp32 operands (M0, R, Delta, T, P) are split into bf16 hi + lo.
 //
-// Every A operand (K, K^T, Q, T, P) comes from a workspace record that k_intra
-// wrote in fragment order, so a compute wave fetches each operand with one
-// conflict-free 16-byte LDS read per lane.  The data wave copies the next
-// chunk's records and value rows global -> LDS by DMA (global_load_lds, 16
-// bytes per lane) into one of two LDS buffers while the compute waves work on
-// the other; the compute waves issue each group of LDS reads one MFMA group
-// ahead of its use, so LDS latency hides behind the matrix cores.
+// Every A operand except P (K, K^T, Q, T) comes from a workspace record that
+// k_intra wrote in fragment order, copied global -> LDS by DMA (global_load_lds,
+// 16 bytes per lane) into one of two LDS buffers while the waves compute on the
+// other; each wave issues an equal share of the next chunk's DMA at the start
+// of a chunk and waits for it at the end.  A wave then fetches each operand
+// with one conflict-free 16-byte LDS read; V uses the transposing LDS read; P
+// (outputs only) comes straight from global memory into registers.  Two waves
+// per SIMD let one wave's VALU work (hi/lo splits) run while the other's MFMAs
+// run.  Inside a chunk the waves issue each group of LDS reads one region
+// ahead of its use.
 #pragma once
 
 #include "gdn_device.h"
@@ -46,31 +48,6 @@ __device__ __forceinline__ int swz(int row, int byte_in_row) {
   return row * ROW_BYTES + 16 * ((byte_in_row / 16) ^ (row % pieces)) + byte_in_row % 16;
 }
 
-constexpr int kComputeWaves = 2;
-constexpr int kScanCols = 16 * kComputeWaves;              // state columns per workgroup
-constexpr int kScanThreads = (kComputeWaves + 1) * kWave;   // + the data wave
-
-// LDS layout of one chunk buffer.
-template <typename TIn, int DK, bool FWD>
-struct ScanLds {
-  static constexpr bool kSplit = sizeof(TIn) == 4;
-  static constexpr int kKFrags = k_record_frags(DK, FWD);         // per bf16 part
-  static constexpr int kKBytes = static_cast<int>(k_record_bytes(DK, FWD, kSplit));
-  static constexpr int kTBytes = static_cast<int>(kTRecordBytes);
-  static constexpr int kPBytes = FWD ? static_cast<int>(kPRecordBytes) : 0;
-  static constexpr int kSBytes = static_cast<int>(kSRecordBytes);
-  static constexpr int kVRowBytes = kScanCols * static_cast<int>(sizeof(TIn));
-  static constexpr int kVBytes = kChunk * kVRowBytes;
-  static constexpr int kOffK = 0;                 // K record
-  static constexpr int kOffT = kOffK + kKBytes;
-  static constexpr int kOffP = kOffT + kTBytes;
-  static constexpr int kOffS = kOffP + kPBytes;
-  static constexpr int kOffV = kOffS + kSBytes;
-  static constexpr int kBytes = kOffV + kVBytes;
-  static constexpr int kBuffers = 2 * kBytes <= kLdsBytes ? 2 : 1;
-  static constexpr int kVBlocks = kVBytes / 1024;
-};
-
 // DMA of rows [0, 64) of a token-major tensor (row 0 at `row0`, 1 KiB block
 // `blk` of the tile) into a swizzled LDS row tile; rows past `rows` repeat the
 // last valid row.
@@ -97,322 +74,515 @@ __device__ __forceinline__ float bf16_elt(const u32x2& x, int j) {
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t out_rsrc(void* base, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(base, 0, bytes, 0x00020000);
 }
-__device__ __forceinline__ void store_out(__amdgpu_buffer_rsrc_t r, int voff, int soff, float x, uint16_t*) {
-  const uint32_t w = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x, 0.f}, bf16x2));
-  __builtin_amdgcn_raw_buffer_store_b16(static_cast<uint16_t>(w), r, voff, soff, 0);
+// Four consecutive output elements of one row, as bf16 (8 bytes) or fp32 (16).
+__device__ __forceinline__ void store_out4(__amdgpu_buffer_rsrc_t r, int voff, const f32x4& x, uint16_t*) {
+  const uint32_t a = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[0], x[1]}, bf16x2));
+  const uint32_t b = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{x[2], x[3]}, bf16x2));
+  __builtin_amdgcn_raw_buffer_store_b64(u32x2{a, b}, r, voff, 0, 0);
 }
-__device__ __forceinline__ void store_out(__amdgpu_buffer_rsrc_t r, int voff, int soff, float x, float*) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x), r, voff, soff, 0);
+__device__ __forceinline__ void store_out4(__amdgpu_buffer_rsrc_t r, int voff, const f32x4& x, float*) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), r, voff, 0, 0);
 }
 
-template <typename TIn, int DK, bool FWD>
-__global__ __launch_bounds__(kScanThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_scan(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
-            const TIn* __restrict__ v,
-            const u32x4* __restrict__ Kw,
-            const u32x4* __restrict__ Tw,
-            const float* __restrict__ Sw,
-            const u32x4* __restrict__ Pw,
-            const float* __restrict__ state_in,
-            TIn* __restrict__ o,
-            float* __restrict__ state_out) {
-  using L = ScanLds<TIn, DK, FWD>;
+// LDS layout of one chunk buffer of a workgroup that covers VC state columns;
+// P (outputs only) is staged in LDS when P_LDS, else read from global memory.
+template <typename TIn, int DK, int VC, bool FWD, bool P_LDS>
+struct ScanLds {
+  static constexpr bool kSplit = sizeof(TIn) == 4;
+  static constexpr bool kPInLds = FWD && P_LDS;
+  static constexpr int kKFrags = k_record_frags(DK, FWD);         // per bf16 part
+  static constexpr int kKBytes = static_cast<int>(k_record_bytes(DK, FWD, kSplit));
+  static constexpr int kTBytes = static_cast<int>(kTRecordBytes);
+  static constexpr int kSBytes = static_cast<int>(kSRecordBytes);
+  static constexpr int kVRowBytes = VC * static_cast<int>(sizeof(TIn));
+  static constexpr int kVBytes = kChunk * kVRowBytes;
+  static constexpr int kOffK = 0;                 // K record
+  static constexpr int kOffT = kOffK + kKBytes;
+  static constexpr int kPBytes = kPInLds ? static_cast<int>(kPRecordBytes) : 0;
+  static constexpr int kOffP = kOffT + kTBytes;
+  static constexpr int kOffS = kOffP + kPBytes;
+  static constexpr int kOffV = kOffS + 2048;      // S padded to two DMA blocks
+  static constexpr int kBytes = kOffV + kVBytes;
+  static constexpr int kBuffers = 2 * kBytes <= kLdsBytes ? 2 : 1;
+  // DMA jobs per chunk (one 1 KiB global_load_lds each): K record, T, P, V
+  // rows, then the scalars as one full and one quarter block
+  static constexpr int kKJobs = kKBytes / 1024, kTJobs = kTBytes / 1024, kPJobs = kPBytes / 1024;
+  static constexpr int kVJobs = kVBytes / 1024;
+  static constexpr int kJobs = kKJobs + kTJobs + kPJobs + kVJobs + 2;
+};
+
+// Where one chunk's operands come from.
+struct ChunkSrc {
+  const unsigned char* krec;   // K record of (slot, key head)
+  const unsigned char* trec;   // T record of (slot, value head)
+  const unsigned char* prec;   // P record of (slot, value head), outputs only
+  const unsigned char* srow;   // scalars of (slot, value head)
+  const void* v0;              // V row 0 of the chunk, first column of the workgroup
+  int clen;                    // valid rows
+};
+
+// DMA job j of a chunk (0 <= j < L::kJobs) into LDS buffer `base`.
+template <typename L, typename TIn>
+__device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, unsigned char* base, int j, int lane) {
+  if (j < L::kKJobs) {
+    dma16(c.krec + 1024 * j + 16 * lane, base + L::kOffK + 1024 * j);
+  } else if (j < L::kKJobs + L::kTJobs) {
+    const int t = j - L::kKJobs;
+    dma16(c.trec + 1024 * t + 16 * lane, base + L::kOffT + 1024 * t);
+  } else if (j < L::kKJobs + L::kTJobs + L::kPJobs) {
+    const int t = j - L::kKJobs - L::kTJobs;
+    dma16(c.prec + 1024 * t + 16 * lane, base + L::kOffP + 1024 * t);
+  } else if (j < L::kKJobs + L::kTJobs + L::kPJobs + L::kVJobs) {
+    // V rows; pad rows repeat the last row (their beta is 0, so they add nothing)
+    dma_rows<L::kVRowBytes>(static_cast<const TIn*>(c.v0), vrow, c.clen, base + L::kOffV,
+                            j - L::kKJobs - L::kTJobs - L::kPJobs, lane);
+  } else if (j == L::kJobs - 2) {
+    dma16(c.srow + 16 * lane, base + L::kOffS);                    // scalars, bytes 0..1023
+  } else if (lane < 16) {
+    dma16(c.srow + 1024 + 16 * lane, base + L::kOffS + 1024);      // bytes 1024..1279
+  }
+}
+
+// One 64-token chunk for one wave: 16 state columns, M (and its split mb) in
+// registers.  `base` is the chunk's LDS buffer, `vc0` the wave's first column
+// within the buffer's V tile, `pg` the chunk's P record in global memory
+// (outputs only, used when the layout does not stage P in LDS).  The chunk runs as a chain of regions: each region issues the
+// LDS reads of a later region, runs MFMAs on operands that are ready, and does
+// VALU work (scaling, hi/lo splits) for the next region that is independent of
+// its own MFMAs.  hook(k) runs at the start of region k (the whole-head kernel
+// issues its DMA share there).  With outputs, the chunk's O is left in `pout`:
+// pout[ti][i] = O[16 ti + lane % 16][4 (lane / 16) + i] of the wave's columns.
+template <typename L, int DK, bool FWD, typename Hook>
+__device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, const u32x4* pg, int lane,
+                                           f32x4 (&M)[DK / 16], Frag (&mb)[DK / 32], f32x4 (&pout)[4],
+                                           Hook&& hook) {
   constexpr bool SPLIT = L::kSplit;
-  constexpr int NT = DK / 16;         // 16-row tiles of M
-  constexpr int NK = DK / 32;         // 32-wide k steps over d_k
+  constexpr int NT = DK / 16, NK = DK / 32;
   constexpr int NKA = ka_frags(DK), NKT = kt_frags(DK);
   constexpr int NKF = L::kKFrags;
   constexpr int VRB = L::kVRowBytes;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+  const int lg = lane / 16, lr = lane % 16;
+  const u32x4* kf = reinterpret_cast<const u32x4*>(base + L::kOffK);
+  const u32x4* tf = reinterpret_cast<const u32x4*>(base + L::kOffT);
+  const float* sc = reinterpret_cast<const float*>(base + L::kOffS);
+  const unsigned char* vtile = base + L::kOffV;
+  // fragment f of the K record (`nf` fragments per bf16 part; the lo part
+  // exists for fp32 inputs only)
+  auto ldf = [&](Frag& x, const u32x4* rec, int f, int nf) __attribute__((always_inline)) {
+    x.hi = __builtin_bit_cast(bf16x8, rec[f * kWave + lane]);
+    if constexpr (SPLIT) x.lo = __builtin_bit_cast(bf16x8, rec[(nf + f) * kWave + lane]);
+  };
+  // fp32-derived records (T, P): always hi and lo
+  auto ld_split = [&](Frag& x, const u32x4* rec, int f) __attribute__((always_inline)) {
+    x.hi = __builtin_bit_cast(bf16x8, rec[f * kWave + lane]);
+    x.lo = __builtin_bit_cast(bf16x8, rec[(kTFrags + f) * kWave + lane]);
+  };
+  // K (and Q) operands of row tiles 2 tp, 2 tp + 1 for every k step
+  auto ld_ka = [&](Frag (&a)[2][NK], Frag (&aq)[2][NK], int tp) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        ldf(a[u][kk], kf, (2 * tp + u) * NK + kk, NKF);
+        if constexpr (FWD) ldf(aq[u][kk], kf, NKA + NKT + (2 * tp + u) * NK + kk, NKF);
+      }
+  };
+  // K^T operands of every row tile of M for k step kk
+  auto ld_kt = [&](Frag (&a)[NT], int kk) __attribute__((always_inline)) {
+#pragma unroll
+    for (int td = 0; td < NT; ++td) ldf(a[td], kf, NKA + 2 * td + kk, NKF);
+  };
 
+  // The chunk runs as a chain of regions.  Each region issues the LDS reads of
+  // a later region, runs MFMAs on operands that are ready, and does VALU work
+  // (scaling, hi/lo splits) for the next region, independent of its own MFMAs
+  // so the two overlap.
+  Frag ka0[2][NK], qa0[2][NK], ka1[2][NK], qa1[2][NK];
+  Frag tfr[kTFrags];
+  Frag kt0[NT], kt1[NT];
+  f32x4 km[4], qm[4], acc[NT], bv[4], R[4], D[4];
+  u32x2 vraw[4];
+  float vf[4][4];
+
+  hook(0);
+  // ---- region 0: first operands
+  ld_ka(ka0, qa0, 0);
+  if constexpr (!SPLIT) {
+    // transposing read: lane (g, c) gets V[16 ti + 4 g + r][c], r = 0..3
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti)
+      vraw[ti] = lds_read_tr16(vtile + swz<VRB>(16 * ti + 4 * lg + lr / 4, 2 * (vc0 + 4 * (lr % 4))));
+  } else {
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        vf[ti][r] = *reinterpret_cast<const float*>(vtile + swz<VRB>(16 * ti + 4 * lg + r, 4 * (vc0 + lr)));
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  hook(1);
+  // ---- region 1: K M0 for row tiles 0, 1 | beta V; the row tiles 2, 3
+  //      operands arrive
+  ld_ka(ka1, qa1, 1);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    km[u] = zero4();
+    qm[u] = zero4();
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      km[u] = mma_a<SPLIT>(ka0[u][kk], mb[kk], km[u]);
+      if constexpr (FWD) qm[u] = mma_b<SPLIT>(mb[kk], qa0[u][kk], qm[u]);
+    }
+  }
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti) {
+    const f32x4 bta = *reinterpret_cast<const f32x4*>(sc + 0 * kChunk + 16 * ti + 4 * lg);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) bv[ti][r] = bta[r] * (SPLIT ? vf[ti][r] : bf16_elt(vraw[ti], r));
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  hook(2);
+  // ---- region 2: K M0 for row tiles 2, 3 | R rows 0..31 and their split;
+  //      T arrives
+#pragma unroll
+  for (int f = 0; f < kTFrags; ++f) ld_split(tfr[f], tf, f);
+#pragma unroll
+  for (int u = 0; u < 2; ++u) {
+    km[2 + u] = zero4();
+    qm[2 + u] = zero4();
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      km[2 + u] = mma_a<SPLIT>(ka1[u][kk], mb[kk], km[2 + u]);
+      if constexpr (FWD) qm[2 + u] = mma_b<SPLIT>(mb[kk], qa1[u][kk], qm[2 + u]);
+    }
+  }
+  auto make_r = [&](int ti) __attribute__((always_inline)) {
+    const f32x4 bge = *reinterpret_cast<const f32x4*>(sc + 1 * kChunk + 16 * ti + 4 * lg);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) R[ti][r] = bv[ti][r] - bge[r] * km[ti][r];
+  };
+  make_r(0);
+  make_r(1);
+  const Frag rb0 = chain_frag(R[0], R[1]);
+  __builtin_amdgcn_sched_barrier(0);
+
+  hook(3);
+  // ---- region 3: Delta = T R, k step 0 for all row tiles | R rows 32..63
+  //      and their split; K^T (k step 0) and P (outputs) arrive
+  ld_kt(kt0, 0);
+  Frag pfr[FWD ? kTFrags : 1];
+  if constexpr (FWD) {
+    // P (fp32-derived: hi and lo parts), staged in LDS or straight from global
+    if constexpr (L::kPInLds) {
+      const u32x4* pl = reinterpret_cast<const u32x4*>(base + L::kOffP);
+#pragma unroll
+      for (int f = 0; f < kTFrags; ++f) ld_split(pfr[f], pl, f);
+    } else {
+#pragma unroll
+      for (int f = 0; f < kTFrags; ++f) {
+        pfr[f].hi = __builtin_bit_cast(bf16x8, pg[f * kWave + lane]);
+        pfr[f].lo = __builtin_bit_cast(bf16x8, pg[(kTFrags + f) * kWave + lane]);
+      }
+    }
+  }
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti) D[ti] = mma_x3(tfr[tri_frag(ti, 0)], rb0, zero4());
+  make_r(2);
+  make_r(3);
+  const Frag rb1 = chain_frag(R[2], R[3]);
+  __builtin_amdgcn_sched_barrier(0);
+
+  hook(4);
+  // ---- region 4: Delta, k step 1 for row tiles 2, 3 | split of the
+  //      weighted Delta rows 0..31 (and of Delta for the outputs); K^T
+  //      arrives
+  ld_kt(kt1, 1);
+#pragma unroll
+  for (int ti = 2; ti < 4; ++ti) D[ti] = mma_x3(tfr[tri_frag(ti, 1)], rb1, D[ti]);
+  f32x4 Dw[4];
+  auto make_dw = [&](int ti) __attribute__((always_inline)) {
+    const f32x4 w = *reinterpret_cast<const f32x4*>(sc + 2 * kChunk + 16 * ti + 4 * lg);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) Dw[ti][r] = w[r] * D[ti][r];
+  };
+  make_dw(0);
+  make_dw(1);
+  const Frag db0 = chain_frag(Dw[0], Dw[1]);
+  Frag dd0;
+  if constexpr (FWD) dd0 = chain_frag(D[0], D[1]);
+  __builtin_amdgcn_sched_barrier(0);
+
+  hook(5);
+  // ---- region 5: M1 partial, k step 0 (tokens 0..31) | split of the
+  //      weighted Delta rows 32..63
+  const float eg = sc[4 * kChunk];
+#pragma unroll
+  for (int td = 0; td < NT; ++td) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc[td][r] = eg * M[td][r];
+    acc[td] = mma_a<SPLIT>(kt0[td], db0, acc[td]);
+  }
+  make_dw(2);
+  make_dw(3);
+  const Frag db1 = chain_frag(Dw[2], Dw[3]);
+  Frag dd1;
+  if constexpr (FWD) dd1 = chain_frag(D[2], D[3]);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- outputs, transposed: O^T = diag-scaled (Q M0)^T + Delta^T P^T, whose
+  //      MFMA layout gives a lane four consecutive columns of one token row
+  //      (row 16 ti + lane % 16, columns 4 (lane / 16) + 0..3 of the wave's 16).
+  //      The split Delta (dd) is the A operand and the P fragments the B
+  //      operand; qm already holds (Q M0)^T (A = split M0, B = Q fragments).
+  //      Stored at the start of the next chunk.
+  if constexpr (FWD) {
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti) {
+      const float qe = sc[3 * kChunk + 16 * ti + lr];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) pout[ti][r] = qe * qm[ti][r];
+      pout[ti] = mma_x3(dd0, pfr[tri_frag(ti, 0)], pout[ti]);
+      if (ti >= 2) pout[ti] = mma_x3(dd1, pfr[tri_frag(ti, 1)], pout[ti]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  hook(6);
+  // ---- region 6: M1, k step 1 (tokens 32..63) | split of M1 for the next chunk
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) {
+    M[2 * kk] = mma_a<SPLIT>(kt1[2 * kk], db1, acc[2 * kk]);
+    M[2 * kk + 1] = mma_a<SPLIT>(kt1[2 * kk + 1], db1, acc[2 * kk + 1]);
+    mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
+  }
+}
+
+// Shared set-up of a scan workgroup for sequence n, value head h, state
+// columns [col0, col0 + VC).
+struct ScanUnit {
+  int n, h, kh, tok0, len, slot0, nch;
+};
+__device__ __forceinline__ ScanUnit scan_unit(const int32_t* __restrict__ cu, int n, int h, int hv, int hk) {
+  ScanUnit u;
+  u.n = n;
+  u.h = h;
+  u.kh = h / (hv / hk);
+  u.tok0 = cu[n];
+  u.len = cu[n + 1] - u.tok0;
+  u.slot0 = u.tok0 / kChunk + n;
+  u.nch = (u.len + kChunk - 1) / kChunk;
+  return u;
+}
+
+template <typename L, typename TIn>
+__device__ __forceinline__ ChunkSrc chunk_src(const ScanUnit& u, int ci, int hk, int hv, int dv, int col0,
+                                              const TIn* v, const u32x4* Kw, const u32x4* Tw,
+                                              const float* Sw, const u32x4* Pw) {
+  const int64_t srec = static_cast<int64_t>(u.slot0 + ci);
+  const int64_t vrow = static_cast<int64_t>(hv) * dv;
+  ChunkSrc c;
+  c.krec = reinterpret_cast<const unsigned char*>(Kw) + (srec * hk + u.kh) * L::kKBytes;
+  c.trec = reinterpret_cast<const unsigned char*>(Tw) + (srec * hv + u.h) * L::kTBytes;
+  c.prec = reinterpret_cast<const unsigned char*>(Pw) + (srec * hv + u.h) * static_cast<int64_t>(kPRecordBytes);
+  c.srow = reinterpret_cast<const unsigned char*>(Sw) + (srec * hv + u.h) * L::kSBytes;
+  c.v0 = v + static_cast<int64_t>(u.tok0 + ci * kChunk) * vrow + static_cast<int64_t>(u.h) * dv + col0;
+  c.clen = min(kChunk, u.len - ci * kChunk);
+  return c;
+}
+
+// Per-wave state load/store and the deferred output store.
+template <int DK>
+__device__ __forceinline__ void load_state(const float* __restrict__ state_in, int64_t sbase, int dv, int lg,
+                                           f32x4 (&M)[DK / 16], Frag (&mb)[DK / 32]) {
+#pragma unroll
+  for (int td = 0; td < DK / 16; ++td)
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+      M[td][r] = state_in ? state_in[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] : 0.f;
+#pragma unroll
+  for (int kk = 0; kk < DK / 32; ++kk) mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
+}
+// Stores a chunk's outputs (`pout` as chunk_step leaves it) for the wave whose
+// first column is `colw`; rows past the chunk's end fall outside the buffer
+// range and are dropped by the hardware.
+template <typename TIn>
+__device__ __forceinline__ void store_chunk_out(TIn* o, const ScanUnit& u, int ci, int hv, int dv, int colw,
+                                                int lane, const f32x4 (&pout)[4]) {
+  constexpr int E = static_cast<int>(sizeof(TIn));
+  const int64_t vrow = static_cast<int64_t>(hv) * dv;
+  const int row_bytes = static_cast<int>(vrow) * E;
+  const int clen = min(kChunk, u.len - ci * kChunk);
+  const __amdgpu_buffer_rsrc_t r =
+      out_rsrc(o + static_cast<int64_t>(u.tok0 + ci * kChunk) * vrow + static_cast<int64_t>(u.h) * dv,
+               clen * row_bytes);
+  const int voff = (lane % 16) * row_bytes + (colw + 4 * (lane / 16)) * E;
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti) store_out4(r, voff + 16 * ti * row_bytes, pout[ti], o);
+}
+
+// ---------------------------------------------------------------- latency kernel
+// grid = N x Hv x d_v/32: two compute waves (16 columns each) and one wave that
+// only issues DMA, one workgroup per CU.  Used when this grid fits on the chip
+// at once, where per-chunk latency is all that matters.
+constexpr int kColsPerGroup = 32;
+constexpr int kColsThreads = 3 * kWave;
+
+template <typename TIn, int DK, bool FWD>
+__global__ __launch_bounds__(kColsThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
+                 const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                 const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
+                 const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
+  using L = ScanLds<TIn, DK, kColsPerGroup, FWD, true>;
+  constexpr int NT = DK / 16;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
   const int tid = threadIdx.x;
   // wave index made provably uniform: DMA destinations (M0) stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const bool data_wave = wave == kComputeWaves;
-  const int lane = tid % kWave;
-  const int lg = lane / 16, lr = lane % 16;
-  const int ngroups = dv / kScanCols;
+  const bool data_wave = wave == 2;
+  const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
+  const int ngroups = dv / kColsPerGroup;
   // logical unit: the column groups of a value head, then the value heads of a
   // key head, are adjacent (same XCD, shared records in its L2)
   const int unit = xcd_remap(blockIdx.x, gridDim.x);
-  const int cgrp = unit % ngroups;
-  const int h = (unit / ngroups) % hv;
-  const int n = unit / (ngroups * hv);
-  const int kh = h / (hv / hk);
-  const int col0 = kScanCols * cgrp;           // first state column of the workgroup
-  const int wcol = 16 * wave + lr;             // this lane's column within the workgroup
-  const int col = col0 + wcol;
-  const int tok0 = cu[n];
-  const int len = cu[n + 1] - tok0;
-  const int slot0 = tok0 / kChunk + n;
-  const int nch = (len + kChunk - 1) / kChunk;
-  const int64_t vrow = static_cast<int64_t>(hv) * dv;   // token stride of v and o
-
-  // ---- the data wave copies chunk ci's operands into LDS buffer b
+  const int col0 = kColsPerGroup * (unit % ngroups);
+  const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
+  const int col = col0 + 16 * wave + lr;
+  const int64_t vrow = static_cast<int64_t>(hv) * dv;
   auto dma_chunk = [&](int ci, int b) __attribute__((always_inline)) {
-    unsigned char* base = lds + b * L::kBytes;
-    const int64_t srec = static_cast<int64_t>(slot0 + ci);
-    const int t0 = tok0 + ci * kChunk;
-    const int clen = min(kChunk, len - ci * kChunk);
-    const unsigned char* krec = reinterpret_cast<const unsigned char*>(Kw) + (srec * hk + kh) * L::kKBytes;
-    const unsigned char* trec = reinterpret_cast<const unsigned char*>(Tw) + (srec * hv + h) * L::kTBytes;
-    const unsigned char* prec = reinterpret_cast<const unsigned char*>(Pw) + (srec * hv + h) * L::kPBytes;
-    // records: 1 KiB blocks copied verbatim, fully unrolled (one DMA each)
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
 #pragma unroll
-    for (int blk = 0; blk < L::kKBytes / 1024; ++blk) dma16(krec + 1024 * blk + 16 * lane, base + L::kOffK + 1024 * blk);
-#pragma unroll
-    for (int blk = 0; blk < L::kTBytes / 1024; ++blk) dma16(trec + 1024 * blk + 16 * lane, base + L::kOffT + 1024 * blk);
-#pragma unroll
-    for (int blk = 0; blk < L::kPBytes / 1024; ++blk) dma16(prec + 1024 * blk + 16 * lane, base + L::kOffP + 1024 * blk);
-    // row scalars: 1280 bytes = one full block and a quarter block
-    const unsigned char* srow = reinterpret_cast<const unsigned char*>(Sw) + (srec * hv + h) * L::kSBytes;
-    dma16(srow + 16 * lane, base + L::kOffS);
-    if (lane < 16) dma16(srow + 1024 + 16 * lane, base + L::kOffS + 1024);
-    // V rows, this workgroup's columns (pad rows repeat the last row; their beta
-    // is 0, so they add nothing)
-    const TIn* v0 = v + static_cast<int64_t>(t0) * vrow + static_cast<int64_t>(h) * dv + col0;
-#pragma unroll
-    for (int blk = 0; blk < L::kVBlocks; ++blk) dma_rows<VRB>(v0, vrow, clen, base + L::kOffV, blk, lane);
+    for (int j = 0; j < L::kJobs; ++j) dma_job<L, TIn>(c, vrow, lds + b * L::kBytes, j, lane);
   };
 
-  // state M (compute waves), accumulator layout: M[td][r] = M[16 td + 4 lg + r][col]
   f32x4 M[NT];
-  const int64_t sbase = (static_cast<int64_t>(n) * hv + h) * DK * dv + col;
-  if (!data_wave && state_in != nullptr) {
-#pragma unroll
-    for (int td = 0; td < NT; ++td)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) M[td][r] = state_in[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv];
-  } else {
-#pragma unroll
-    for (int td = 0; td < NT; ++td) M[td] = zero4();
-  }
-  // M split into bf16 hi/lo as the B operand of K M0 (and Q M0), one per k step;
-  // refreshed at the end of every chunk's state update
-  Frag mb[NK];
-#pragma unroll
-  for (int kk = 0; kk < NK; ++kk) mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
+  Frag mb[DK / 32];
+  f32x4 pout[4];
+  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * dv + col;
+  if (!data_wave) load_state<DK>(state_in, sbase, dv, lg, M, mb);
 
-  if (data_wave && nch > 0) {
+  if (data_wave && u.nch > 0) {
     dma_chunk(0, 0);
     wait_dma();
   }
   __syncthreads();
-
-  for (int ci = 0; ci < nch; ++ci) {
+  for (int ci = 0; ci < u.nch; ++ci) {
     const int b = L::kBuffers == 2 ? (ci & 1) : 0;
     if (data_wave) {
-      if (L::kBuffers == 2 && ci + 1 < nch) {
+      if (L::kBuffers == 2 && ci + 1 < u.nch) {
         dma_chunk(ci + 1, b ^ 1);   // lands while the compute waves work on buffer b
         wait_dma();
       }
     } else {
-      const unsigned char* base = lds + b * L::kBytes;
-      const u32x4* kf = reinterpret_cast<const u32x4*>(base + L::kOffK);
-      const u32x4* tf = reinterpret_cast<const u32x4*>(base + L::kOffT);
-      const u32x4* pf = reinterpret_cast<const u32x4*>(base + L::kOffP);
-      const float* sc = reinterpret_cast<const float*>(base + L::kOffS);
-      const unsigned char* vtile = base + L::kOffV;
-      const int t0 = tok0 + ci * kChunk;
-      const int clen = min(kChunk, len - ci * kChunk);
-      // fragment f of the K record (`nf` fragments per bf16 part; the lo part
-      // exists for fp32 inputs only)
-      auto ldf = [&](Frag& x, const u32x4* rec, int f, int nf) __attribute__((always_inline)) {
-        x.hi = __builtin_bit_cast(bf16x8, rec[f * kWave + lane]);
-        if constexpr (SPLIT) x.lo = __builtin_bit_cast(bf16x8, rec[(nf + f) * kWave + lane]);
-      };
-      // fp32-derived records (T, P): always hi and lo
-      auto ld_split = [&](Frag& x, const u32x4* rec, int f) __attribute__((always_inline)) {
-        x.hi = __builtin_bit_cast(bf16x8, rec[f * kWave + lane]);
-        x.lo = __builtin_bit_cast(bf16x8, rec[(kTFrags + f) * kWave + lane]);
-      };
-      // K (and Q) operands of row tiles 2 tp, 2 tp + 1 for every k step
-      auto ld_ka = [&](Frag (&a)[2][NK], Frag (&aq)[2][NK], int tp) __attribute__((always_inline)) {
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-          for (int kk = 0; kk < NK; ++kk) {
-            ldf(a[u][kk], kf, (2 * tp + u) * NK + kk, NKF);
-            if constexpr (FWD) ldf(aq[u][kk], kf, NKA + NKT + (2 * tp + u) * NK + kk, NKF);
-          }
-      };
-      // K^T operands of every row tile of M for k step kk
-      auto ld_kt = [&](Frag (&a)[NT], int kk) __attribute__((always_inline)) {
-#pragma unroll
-        for (int td = 0; td < NT; ++td) ldf(a[td], kf, NKA + 2 * td + kk, NKF);
-      };
-
-      // The chunk runs as a chain of regions.  Each region issues the LDS reads of
-      // a later region, runs MFMAs on operands that are ready, and does VALU work
-      // (scaling, hi/lo splits) for the next region, independent of its own MFMAs
-      // so the two overlap.
-      Frag ka0[2][NK], qa0[2][NK], ka1[2][NK], qa1[2][NK];
-      Frag tfr[kTFrags], pfr[FWD ? kTFrags : 1];
-      Frag kt0[NT], kt1[NT];
-      f32x4 km[4], qm[4], acc[NT], bv[4], R[4], D[4];
-      u32x2 vraw[4];
-      float vf[4][4];
-
-      // ---- region 0: first operands
-      ld_ka(ka0, qa0, 0);
-      if constexpr (!SPLIT) {
-        // transposing read: lane (g, c) gets V[16 ti + 4 g + r][c], r = 0..3
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti)
-          vraw[ti] = lds_read_tr16(vtile + swz<VRB>(16 * ti + 4 * lg + lr / 4, 2 * (16 * wave + 4 * (lr % 4))));
-      } else {
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti)
-#pragma unroll
-          for (int r = 0; r < 4; ++r)
-            vf[ti][r] = *reinterpret_cast<const float*>(vtile + swz<VRB>(16 * ti + 4 * lg + r, 4 * wcol));
-      }
-      ld_ka(ka1, qa1, 1);
-      __builtin_amdgcn_sched_barrier(0);
-
-      // ---- region 1: K M0 for row tiles 0, 1 | beta V, e^{G_last} M0
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        km[u] = zero4();
-        qm[u] = zero4();
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
-          km[u] = mma_a<SPLIT>(ka0[u][kk], mb[kk], km[u]);
-          if constexpr (FWD) qm[u] = mma_a<SPLIT>(qa0[u][kk], mb[kk], qm[u]);
-        }
-      }
-      {
-        const float eg = sc[4 * kChunk];
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti) {
-          const f32x4 bta = *reinterpret_cast<const f32x4*>(sc + 0 * kChunk + 16 * ti + 4 * lg);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) bv[ti][r] = bta[r] * (SPLIT ? vf[ti][r] : bf16_elt(vraw[ti], r));
-        }
-#pragma unroll
-        for (int td = 0; td < NT; ++td)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) acc[td][r] = eg * M[td][r];
-      }
-      __builtin_amdgcn_sched_barrier(0);
-
-      // ---- region 2: K M0 for row tiles 2, 3 | R rows 0..31 and their split;
-      //      T arrives
-#pragma unroll
-      for (int f = 0; f < kTFrags; ++f) ld_split(tfr[f], tf, f);
-#pragma unroll
-      for (int u = 0; u < 2; ++u) {
-        km[2 + u] = zero4();
-        qm[2 + u] = zero4();
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
-          km[2 + u] = mma_a<SPLIT>(ka1[u][kk], mb[kk], km[2 + u]);
-          if constexpr (FWD) qm[2 + u] = mma_a<SPLIT>(qa1[u][kk], mb[kk], qm[2 + u]);
-        }
-      }
-      auto make_r = [&](int ti) __attribute__((always_inline)) {
-        const f32x4 bge = *reinterpret_cast<const f32x4*>(sc + 1 * kChunk + 16 * ti + 4 * lg);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) R[ti][r] = bv[ti][r] - bge[r] * km[ti][r];
-      };
-      make_r(0);
-      make_r(1);
-      const Frag rb0 = chain_frag(R[0], R[1]);
-      __builtin_amdgcn_sched_barrier(0);
-
-      // ---- region 3: Delta = T R, k step 0 for all row tiles | R rows 32..63
-      //      and their split; K^T (k step 0) arrives
-      ld_kt(kt0, 0);
-#pragma unroll
-      for (int ti = 0; ti < 4; ++ti) D[ti] = mma_x3(tfr[tri_frag(ti, 0)], rb0, zero4());
-      make_r(2);
-      make_r(3);
-      const Frag rb1 = chain_frag(R[2], R[3]);
-      __builtin_amdgcn_sched_barrier(0);
-
-      // ---- region 4: Delta, k step 1 for row tiles 2, 3 | split of the
-      //      weighted Delta rows 0..31 (and of Delta for the outputs); K^T
-      //      arrives
-      ld_kt(kt1, 1);
-#pragma unroll
-      for (int ti = 2; ti < 4; ++ti) D[ti] = mma_x3(tfr[tri_frag(ti, 1)], rb1, D[ti]);
-      f32x4 Dw[4];
-      auto make_dw = [&](int ti) __attribute__((always_inline)) {
-        const f32x4 w = *reinterpret_cast<const f32x4*>(sc + 2 * kChunk + 16 * ti + 4 * lg);
-#pragma unroll
-        for (int r = 0; r < 4; ++r) Dw[ti][r] = w[r] * D[ti][r];
-      };
-      make_dw(0);
-      make_dw(1);
-      const Frag db0 = chain_frag(Dw[0], Dw[1]);
-      Frag dd0;
-      if constexpr (FWD) dd0 = chain_frag(D[0], D[1]);
-      __builtin_amdgcn_sched_barrier(0);
-
-      // ---- region 5: M1 partial, k step 0 (tokens 0..31) | split of the
-      //      weighted Delta rows 32..63; P (outputs) arrives
       if constexpr (FWD) {
-#pragma unroll
-        for (int f = 0; f < kTFrags; ++f) ld_split(pfr[f], pf, f);
+        if (ci > 0) store_chunk_out(o, u, ci - 1, hv, dv, col - lr, lane, pout);
       }
-#pragma unroll
-      for (int td = 0; td < NT; ++td) acc[td] = mma_a<SPLIT>(kt0[td], db0, acc[td]);
-      make_dw(2);
-      make_dw(3);
-      const Frag db1 = chain_frag(Dw[2], Dw[3]);
-      Frag dd1;
-      if constexpr (FWD) dd1 = chain_frag(D[2], D[3]);
-      __builtin_amdgcn_sched_barrier(0);
-
-      // ---- outputs O = scale e^G (Q M0) + P Delta; rows past the chunk's end
-      //      fall outside the buffer range and are not written
-      if constexpr (FWD) {
-        constexpr int E = static_cast<int>(sizeof(TIn));
-        const int row_bytes = static_cast<int>(vrow) * E;
-        const __amdgpu_buffer_rsrc_t orsrc =
-            out_rsrc(o + static_cast<int64_t>(t0) * vrow + static_cast<int64_t>(h) * dv, clen * row_bytes);
-        const int voff = 4 * lg * row_bytes + col * E;
-        f32x4 out[4];
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti) {
-          const f32x4 qe = *reinterpret_cast<const f32x4*>(sc + 3 * kChunk + 16 * ti + 4 * lg);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) out[ti][r] = qe[r] * qm[ti][r];
-          out[ti] = mma_x3(pfr[tri_frag(ti, 0)], dd0, out[ti]);
-          if (ti >= 2) out[ti] = mma_x3(pfr[tri_frag(ti, 1)], dd1, out[ti]);
-        }
-#pragma unroll
-        for (int ti = 0; ti < 4; ++ti)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) store_out(orsrc, voff + (16 * ti + r) * row_bytes, 0, out[ti][r], o);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-
-      // ---- region 6: M1, k step 1 (tokens 32..63) | split of M1 for the next chunk
-#pragma unroll
-      for (int kk = 0; kk < NK; ++kk) {
-        M[2 * kk] = mma_a<SPLIT>(kt1[2 * kk], db1, acc[2 * kk]);
-        M[2 * kk + 1] = mma_a<SPLIT>(kt1[2 * kk + 1], db1, acc[2 * kk + 1]);
-        mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
-      }
+      const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
+      chunk_step<L, DK, FWD>(lds + b * L::kBytes, 16 * wave, pg, lane, M, mb, pout, [](int) {});
     }
-
     if (L::kBuffers == 1) {
       __syncthreads();   // the compute waves are done with the only buffer
-      if (data_wave && ci + 1 < nch) {
+      if (data_wave && ci + 1 < u.nch) {
         dma_chunk(ci + 1, 0);
         wait_dma();
       }
     }
     __syncthreads();     // next chunk's operands are in LDS; this buffer is free
   }
+  if (!data_wave) {
+    if constexpr (FWD) {
+      if (u.nch > 0) store_chunk_out(o, u, u.nch - 1, hv, dv, col - lr, lane, pout);
+    }
+    if (state_out) {
+#pragma unroll
+      for (int td = 0; td < NT; ++td)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] = M[td][r];
+    }
+  }
+}
 
-  if (!data_wave && state_out) {
+// ---------------------------------------------------------------- throughput kernel
+// grid = N x Hv: d_v/16 waves (two per SIMD for d_v = 128), each 16 columns,
+// sharing one copy of the chunk's records per head; every wave issues an equal
+// share of the next chunk's DMA, spread over the chunk's regions.  Used when
+// the latency kernel's grid would not fit on the chip at once.
+constexpr int head_threads(int dv) { return dv / 16 * kWave; }
+
+template <typename TIn, int DK, int DV, bool FWD>
+__global__ __launch_bounds__(head_threads(DV))
+void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
+                 const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                 const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
+                 const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
+  using L = ScanLds<TIn, DK, DV, FWD, false>;
+  constexpr int NT = DK / 16;
+  constexpr int W = DV / 16;
+  constexpr int PER_WAVE = (L::kJobs + W - 1) / W;   // DMA jobs per wave per chunk
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
+  // logical unit: the value heads of a key head are adjacent (same XCD)
+  const int unit = xcd_remap(blockIdx.x, gridDim.x);
+  const ScanUnit u = scan_unit(cu, unit / hv, unit % hv, hv, hk);
+  const int col = 16 * wave + lr;
+  const int64_t vrow = static_cast<int64_t>(hv) * DV;
+  // jobs wave + W * jj, jj in [j0, j1), of chunk ci into buffer b
+  auto dma_share = [&](int ci, int b, int j0, int j1) __attribute__((always_inline)) {
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, DV, 0, v, Kw, Tw, Sw, Pw);
+#pragma unroll
+    for (int jj = j0; jj < j1; ++jj) {
+      const int j = wave + W * jj;
+      if (j < L::kJobs) dma_job<L, TIn>(c, vrow, lds + b * L::kBytes, j, lane);
+    }
+  };
+
+  f32x4 M[NT];
+  Frag mb[DK / 32];
+  f32x4 pout[4];
+  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * DV + col;
+  load_state<DK>(state_in, sbase, DV, lg, M, mb);
+
+  if (u.nch > 0) {
+    dma_share(0, 0, 0, PER_WAVE);
+    wait_dma();
+  }
+  __syncthreads();
+  for (int ci = 0; ci < u.nch; ++ci) {
+    const int b = L::kBuffers == 2 ? (ci & 1) : 0;
+    if constexpr (FWD) {
+      if (ci > 0) store_chunk_out(o, u, ci - 1, hv, DV, col - lr, lane, pout);
+    }
+    const bool prefetch = L::kBuffers == 2 && ci + 1 < u.nch;
+    // the next chunk's DMA share, a few jobs at the start of each region
+    auto hook = [&](int k) __attribute__((always_inline)) {
+      if (prefetch) {
+        const int j0 = k * PER_WAVE / 7, j1 = (k + 1) * PER_WAVE / 7;
+        if (j1 > j0) dma_share(ci + 1, b ^ 1, j0, j1);
+      }
+    };
+    const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
+    chunk_step<L, DK, FWD>(lds + b * L::kBytes, 16 * wave, pg, lane, M, mb, pout, hook);
+    if (L::kBuffers == 1) {
+      __syncthreads();   // every wave is done with the only buffer
+      if (ci + 1 < u.nch) dma_share(ci + 1, 0, 0, PER_WAVE);
+    }
+    wait_dma();          // this wave's share of the next chunk has landed
+    __syncthreads();     // ... and everyone else's; this chunk's buffer is free
+  }
+  if constexpr (FWD) {
+    if (u.nch > 0) store_chunk_out(o, u, u.nch - 1, hv, DV, col - lr, lane, pout);
+  }
+  if (state_out) {
 #pragma unroll
     for (int td = 0; td < NT; ++td)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] = M[td][r];
+        state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * DV] = M[td][r];
   }
 }
 

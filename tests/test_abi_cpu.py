@@ -133,7 +133,7 @@ def test_tail_replay_rejects_before_launch(case):
 
 
 @needs_no_gpu
-@pytest.mark.parametrize("case", ["null_q", "null_o", "overlap", "small_ws"])
+@pytest.mark.parametrize("case", ["null_q", "null_o", "overlap", "small_ws", "misaligned_o"])
 def test_chunk_forward_rejects_before_launch(case):
     lib = gdn.load_library()
     shape = _shape(num_seqs=2)
@@ -144,10 +144,11 @@ def test_chunk_forward_rejects_before_launch(case):
     s_out = ctypes.c_void_p(0x100000 + (state_bytes // 2 if case == "overlap" else 2 * state_bytes))
     st = lib.gdn_chunk_forward(ctypes.byref(shape), ctypes.cast(cu_host, ctypes.c_void_p), FAKE,
                                None if case == "null_q" else FAKE, FAKE, FAKE, FAKE, FAKE,
-                               s_in, None if case == "null_o" else FAKE, s_out,
+                               s_in, None if case == "null_o" else
+                               (ctypes.c_void_p(0x1008) if case == "misaligned_o" else FAKE), s_out,
                                ctypes.c_void_p(0x20000),
                                need - 256 if case == "small_ws" else need, None)
-    want = {"null_q": 1, "null_o": 1, "overlap": 2, "small_ws": 5}[case]
+    want = {"null_q": 1, "null_o": 1, "overlap": 2, "small_ws": 5, "misaligned_o": 4}[case]
     assert st == want, lib.gdn_last_error().decode()
 
 

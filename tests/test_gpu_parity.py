@@ -59,6 +59,32 @@ def test_ragged_varlen(dtype, dk, dv, grp):
     assert torch.equal(st2[0], torch.from_numpy(s0[0]).cuda())
 
 
+# 72 short sequences: with 4 value heads the column-split grid is 72 x 4 x d_v/32
+# >= 576 workgroups, more than the 256 CUs, so the whole-head scan kernel runs
+WIDE_LENS = [1 + (37 * i) % 200 for i in range(72)]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("dk,dv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+def test_wide_batch_whole_head_kernel(dtype, dk, dv):
+    shape = synth.Shape(hk=2, hv=4, dk=dk, dv=dv, dtype=dtype)
+    seqs = [synth.tokens(101, 0, i, 0, n, shape) for i, n in enumerate(WIDE_LENS)]
+    p = synth.pack(seqs)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    _, want = oracle_run(p)
+    e_tail = state_err(to_f64(st), want)
+    rng = np.random.default_rng(8)
+    s0 = (rng.standard_normal((len(WIDE_LENS), shape.hv, dk, dv)) * 0.3).astype(np.float32)
+    o, st2 = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                               state_in=torch.from_numpy(s0).cuda(), scale=0.5)
+    wo, ws = oracle_run(p, state_in=s0.astype(np.float64), outputs=True, scale=0.5)
+    e_st = state_err(to_f64(st2), ws)
+    e_o = output_err(to_f64(o), wo, p.cu_seqlens)
+    _report(f"wide {dtype} dk={dk} dv={dv}", tail=e_tail, fwd_state=e_st, out=e_o)
+    assert e_tail <= STATE_TOL and e_st <= STATE_TOL and e_o <= OUTPUT_TOL
+
+
 def _chain(shape, hits, outputs_scale=1.0):
     """GPU: tail replay then suffix forward from the rebuilt state; the oracle
     does the same chain in fp64.  Returns the error triple."""
