@@ -11,11 +11,15 @@ Default workload: one GDN layer with hybrid-model head shapes (16 key heads,
 prefix 8192 tokens, replay tail 819 tokens (10 %), 512 suffix tokens.
 
 Prints ONE JSON line.  ``value`` is tokens through the path per second
-(tail + suffix tokens per step / step time), launched eagerly on one stream
-(``ms_per_step_graph`` gives the same step replayed from a HIP graph).  Per-stage
-kernel durations come from HIP events that the library records between its
-kernels on the stream the kernels run on, in a separate pass of the same
-steps; ``roofline`` describes the dominant kernel.
+(tail + suffix tokens per step / step time): the step is one
+``gdn_replay_forward`` call (replay, then the suffix forward from the rebuilt
+state, the suffix's chunk preparation overlapped with the tail's scan),
+launched eagerly on one stream.  ``ms_per_step_two_calls`` times the same work
+as ``gdn_tail_replay`` + ``gdn_chunk_forward``, ``ms_per_step_graph`` the fused
+step replayed from a HIP graph.  Per-stage kernel durations come from HIP
+events that the library records between its kernels on the stream the kernels
+run on, in a separate pass of the same steps; ``roofline`` describes the
+dominant kernel.
 
 ``--summarize-pmc FETCH_DIR WRITE_DIR`` (no GPU) turns two rocprofv3 --pmc
 runs of ``bench.py --calib-copy`` (FETCH_SIZE, then WRITE_SIZE) into the
@@ -230,8 +234,12 @@ def main():
     ws_f = torch.empty(gdn.workspace_size(N, hk, hv, dk, dv, suf.cu_seqlens.tolist(),
                                           with_outputs=True) + 256,
                        dtype=torch.uint8, device=dev)
+    ws_rf = torch.empty(gdn.replay_forward_workspace_size(N, hk, hv, dk, dv, tail.cu_seqlens.tolist(),
+                                                          suf.cu_seqlens.tolist()) + 256,
+                        dtype=torch.uint8, device=dev)
     names_t = gdn.stage_names(False)
     names_f = gdn.stage_names(True)
+    names_rf = gdn.replay_forward_stage_names()
 
     def new_events(n):
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
@@ -247,12 +255,19 @@ def main():
         gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
                           state_in=state, o=o, state_out=state2, workspace=ws_f, events=ev)
 
-    def step(ev_t=None, ev_f=None):
+    def two_calls(ev_t=None, ev_f=None):
         replay_call(ev_t)
         forward_call(ev_f)
 
+    def step(ev=None):
+        gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xs["q"], xs["k"], xs["v"],
+                           xs["g"], xs["beta"], xs["cu"], cu_tail_host=xt["cu_host"],
+                           cu_suf_host=xs["cu_host"], state_mid=state, o=o, state_out=state2,
+                           workspace=ws_rf, events=ev)
+
     for _ in range(args.warmup):
         step()
+        two_calls()
     torch.cuda.synchronize()
     K = args.steps
 
@@ -287,20 +302,27 @@ def main():
         if ok:
             graph = g
         else:
-            graph_note = "graph replay differed from the eager step; timed eagerly"
+            graph_note = "graph replay differed from the eager step; graph not timed"
 
     ms_per_step = timed(step)
+    ms_two = timed(two_calls)
     ms_graph = timed(graph.replay) if graph is not None else None
 
     # ---- per-stage kernel durations: events recorded by the library on its stream
+    ev_rf = [new_events(len(names_rf) + 1) for _ in range(K)]
+    torch.cuda.synchronize()
+    for i in range(K):
+        step(ev_rf[i])
+    torch.cuda.synchronize()
     ev_t = [new_events(len(names_t) + 1) for _ in range(K)]
     ev_f = [new_events(len(names_f) + 1) for _ in range(K)]
     torch.cuda.synchronize()
     for i in range(K):
-        step(ev_t[i], ev_f[i])
+        two_calls(ev_t[i], ev_f[i])
     torch.cuda.synchronize()
     stages = {}
-    for prefix, names, evs in (("tail_replay", names_t, ev_t), ("chunk_forward", names_f, ev_f)):
+    for prefix, names, evs in (("replay_forward", names_rf, ev_rf), ("tail_replay", names_t, ev_t),
+                               ("chunk_forward", names_f, ev_f)):
         for j, nm in enumerate(names):
             d = [evs[i][j].elapsed_time(evs[i][j + 1]) * 1e3 for i in range(K)]
             stages[f"{prefix}.{nm}"] = {"mean_us": statistics.fmean(d),
@@ -344,18 +366,19 @@ def main():
     t_s = ms_per_step * 1e-3
     path_bound_s = max(path_flops / (BF16_PEAK_TFLOPS * 1e12), path_bytes / (HBM_PEAK_GBS * 1e9))
 
-    # dominant kernel: the stage with the largest mean time per step; its
-    # algorithmic bytes are those of the call it belongs to
-    dom = max(stages, key=lambda k: stages[k]["mean_us"])
-    dom_call = dom.split(".")[0]
-    kbytes = tail_bytes if dom_call == "tail_replay" else fwd_bytes
-    kflops = tail_flops if dom_call == "tail_replay" else fwd_flops
+    # dominant kernel: the stage of the timed (fused) step with the largest
+    # mean time; its algorithmic bytes are those of the part of the path it
+    # runs (the tail replay's or the suffix forward's)
+    fused = {k: v for k, v in stages.items() if k.startswith("replay_forward.")}
+    dom = max(fused, key=lambda k: fused[k]["mean_us"])
+    on_tail = dom in ("replay_forward.tail intra", "replay_forward.tail scan + suffix intra")
+    kbytes = tail_bytes if on_tail else fwd_bytes
+    kflops = tail_flops if on_tail else fwd_flops
     dom_s = stages[dom]["mean_us"] * 1e-6
     achieved = kbytes / dom_s / 1e9
-    kname = {"tail_replay.scan": "gdn::k_scan<unsigned short, 128, false>",
-             "chunk_forward.scan": "gdn::k_scan<unsigned short, 128, true>",
-             "tail_replay.intra": "gdn::k_intra<unsigned short, 128, false>",
-             "chunk_forward.intra": "gdn::k_intra<unsigned short, 128, true>"}.get(dom)
+    kname = {"replay_forward.tail intra": "gdn::k_intra<unsigned short, 128, false>",
+             "replay_forward.tail scan + suffix intra": "gdn::k_scan_cols_intra<unsigned short, 128>",
+             "replay_forward.suffix scan": "gdn::k_scan_cols<unsigned short, 128, true>"}.get(dom)
     traffic = load_traffic(args.replay, kname) if kname else None
     roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                 "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
@@ -380,7 +403,8 @@ def main():
                                f"prefix 8192, tail replay r={r} from zero + {s}-token suffix "
                                f"forward with outputs",
                    "global_batch": 1, "seq_len": r + s, "parallelism": "single GPU"},
-        "launch": "eager",
+        "launch": "eager, gdn_replay_forward",
+        "ms_per_step_two_calls": ms_two,
         "ms_per_step_graph": ms_graph,
         "rebuild_latency_us": warm["p50"],
         "rebuild_latency_warm_us": warm,
@@ -467,6 +491,16 @@ def sweep(args):
                           state_in=state_in, o=o, state_out=state_out, workspace=ws,
                           write_state=write_state)
 
+    def fused(xt, xs, st, o, st2, ws):
+        gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xs["q"], xs["k"], xs["v"],
+                           xs["g"], xs["beta"], xs["cu"], cu_tail_host=xt["cu_host"],
+                           cu_suf_host=xs["cu_host"], state_mid=st, o=o, state_out=st2, workspace=ws)
+
+    def fused_ws(xt, xs, n, hk, hv, d):
+        return torch.empty(gdn.replay_forward_workspace_size(n, hk, hv, d, d, xt["cu_host"].tolist(),
+                                                             xs["cu_host"].tolist(), dtype=xt["k"].dtype)
+                           + 256, dtype=torch.uint8, device=dev)
+
     def buffers(x, n, hk, hv, d, outputs):
         cu = x["cu_host"].tolist()
         ws = torch.empty(gdn.workspace_size(n, hk, hv, d, d, cu, dtype=x["k"].dtype,
@@ -485,10 +519,13 @@ def sweep(args):
     xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
     wst, st, _ = buffers(xt, 1, 4, 4, 64, False)
     wsf, st2, o = buffers(xs, 1, 4, 4, 64, True)
+    wsr = fused_ws(xt, xs, 1, 4, 4, 64)
     rep = timed_us(lambda: replay(xt, st, wst))
-    both = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
     emit({"workload": "small fp32 layer Hk=Hv=4 d=64: tail 205 + suffix 256",
-          "rebuild_latency_us": rep, "step_us": both, "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
+          "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+          "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
 
     # ---- hybrid-model layer, tail 410 (the default bench line covers 819)
     shape, hits = workloads.workload1(410)
@@ -496,10 +533,13 @@ def sweep(args):
     xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
     wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
     wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
+    wsr = fused_ws(xt, xs, 1, 16, 32, 128)
     rep = timed_us(lambda: replay(xt, st, wst))
-    both = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
     emit({"workload": "one GDN layer Hk=16 Hv=32 d=128 bf16: tail 410 + suffix 512",
-          "rebuild_latency_us": rep, "step_us": both, "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
+          "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+          "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
 
     # ---- 36-layer stack, m = 32768, r = 3277: 36 sequential per-layer replays,
     #      and the batched variant (layers as 36 sequences of one launch)
@@ -524,15 +564,19 @@ def sweep(args):
     n = len(hits)
     wst, st, _ = buffers(xt, n, 16, 32, 128, False)
     wsf, st2, o = buffers(xs, n, 16, 32, 128, True)
+    wsr = fused_ws(xt, xs, n, 16, 32, 128)
     rep = timed_us(lambda: replay(xt, st, wst))
-    both = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+    both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
     sr, ss = sum(h.r for h in hits), sum(h.s for h in hits)
     emit({"workload": f"16 varlen hits Hk=16 Hv=32 d=128 bf16: sum r={sr}, sum s={ss}",
-          "rebuild_latency_us": rep, "step_us": both, "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
+          "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+          "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
           "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
 
     # ---- replay vs full prefill, suffix 512: t_full = forward(0, m + s) with
-    #      outputs; t_replay = replay(r) + forward(S_m, s); state-only full = replay(m + s)
+    #      outputs; t_replay = the fused replay(r) + forward(S_m, s); state-only
+    #      full = replay(m + s)
     for m in (8192, 16384, 32768):
         x_full = random_dev([m + 512], 16, 32, 128, seed=m)
         wsF, stF, oF = buffers(x_full, 1, 16, 32, 128, True)
@@ -544,9 +588,11 @@ def sweep(args):
             r = {(8192, "0.1"): 819, (32768, "0.05"): 1638}.get((m, pct), gdn.replay_len(m, pct))
             xt = random_dev([r], 16, 32, 128, seed=m + r)
             xs = random_dev([512], 16, 32, 128, seed=m + 1)
-            wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
-            wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
-            t_rep = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+            st = torch.empty((1, 32, 128, 128), dtype=torch.float32, device=dev)
+            st2 = torch.empty_like(st)
+            o = torch.empty((512, 32, 128), dtype=torch.bfloat16, device=dev)
+            wsr = fused_ws(xt, xs, 1, 16, 32, 128)
+            t_rep = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
             emit({"workload": f"replay vs full prefill Hk=16 Hv=32 d=128 bf16, m={m}, r={r}, suffix 512",
                   "t_full_us": t_full["p50"], "t_full_state_only_us": t_state["p50"],
                   "t_replay_us": t_rep["p50"], "speedup": t_full["p50"] / t_rep["p50"],

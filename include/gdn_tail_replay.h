@@ -153,6 +153,56 @@ int32_t gdn_num_stages(int32_t with_outputs);
 const char* gdn_stage_name(int32_t with_outputs, int32_t stage);
 
 /*
+ * Replay, then continue (paper Section 3: the rebuilt state S_m is the start
+ * of the new suffix's prefill, Eq. 2 followed by Eq. 1 from i = m + 1).  One
+ * call does what gdn_tail_replay followed by gdn_chunk_forward(state_in =
+ * state_mid) does, with the same results bit for bit, but overlaps work that
+ * does not depend on the rebuilt state: the suffix's per-chunk preparation
+ * runs beside the tail's sequential scan.
+ *   tail   (sequence n = the last r_n matched tokens, packed by cu_tail):
+ *          k_tail [Tt,Hk,d_k], v_tail [Tt,Hv,d_v], g_tail, beta_tail [Tt,Hv];
+ *   suffix (the new tokens of sequence n, packed by cu_suf, same N):
+ *          q, k [Ts,Hk,d_k], v [Ts,Hv,d_v], g, beta [Ts,Hv];
+ *   state_mid [N,Hv,d_k,d_v]: receives S_m, the replayed state (required);
+ *   o [Ts,Hv,d_v]: suffix outputs; state_out: final state (NULL = not
+ *   written; may equal state_mid, must not otherwise overlap it).
+ * workspace: at least gdn_replay_forward_workspace_size(...) bytes, 256-byte
+ * aligned.  Validation and errors as for the two separate calls.
+ */
+gdn_status gdn_replay_forward_workspace_size(const gdn_shape* shape,
+                                             const int32_t* cu_tail_host,
+                                             const int32_t* cu_suf_host,
+                                             size_t* bytes);
+
+gdn_status gdn_replay_forward(const gdn_shape* shape,
+                              const int32_t* cu_tail_host, const int32_t* cu_tail,
+                              const void* k_tail, const void* v_tail,
+                              const float* g_tail, const float* beta_tail,
+                              const int32_t* cu_suf_host, const int32_t* cu_suf,
+                              const void* q, const void* k, const void* v,
+                              const float* g, const float* beta,
+                              float* state_mid, void* o, float* state_out,
+                              void* workspace, size_t workspace_bytes,
+                              void* stream);
+
+/* Profiling variant of gdn_replay_forward, events as for the other calls;
+ * num_events must be gdn_replay_forward_num_stages() + 1. */
+gdn_status gdn_replay_forward_profiled(const gdn_shape* shape,
+                                       const int32_t* cu_tail_host, const int32_t* cu_tail,
+                                       const void* k_tail, const void* v_tail,
+                                       const float* g_tail, const float* beta_tail,
+                                       const int32_t* cu_suf_host, const int32_t* cu_suf,
+                                       const void* q, const void* k, const void* v,
+                                       const float* g, const float* beta,
+                                       float* state_mid, void* o, float* state_out,
+                                       void* workspace, size_t workspace_bytes,
+                                       void* stream,
+                                       void* const* stage_events, int32_t num_events);
+
+int32_t gdn_replay_forward_num_stages(void);
+const char* gdn_replay_forward_stage_name(int32_t stage);
+
+/*
  * Replay budget of the paper (Section 3): k = ceil(r * m) for a ratio
  * r = ratio_num / ratio_den, in exact integer arithmetic.  Returns -1 when
  * m < 0, ratio_num < 0, ratio_den <= 0 or the product overflows.

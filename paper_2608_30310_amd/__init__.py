@@ -7,8 +7,10 @@ suffix and emit its outputs.  The work runs in hand-written HIP kernels for
 gfx950 behind the C ABI declared in ``include/gdn_tail_replay.h``; this
 package is a thin binding of that library.
 """
-from .binding import (GDNError, LIB_PATH, chunk_forward, load_library, replay_len,
+from .binding import (GDNError, LIB_PATH, chunk_forward, load_library, replay_forward,
+                      replay_forward_stage_names, replay_forward_workspace_size, replay_len,
                       stage_names, tail_replay, workspace_size)
 
-__all__ = ["GDNError", "LIB_PATH", "chunk_forward", "load_library", "replay_len",
+__all__ = ["GDNError", "LIB_PATH", "chunk_forward", "load_library", "replay_forward",
+           "replay_forward_stage_names", "replay_forward_workspace_size", "replay_len",
            "stage_names", "tail_replay", "workspace_size"]

@@ -62,6 +62,16 @@ def load_library():
     lib.gdn_tail_replay_profiled.restype = ctypes.c_int
     lib.gdn_chunk_forward_profiled.argtypes = lib.gdn_chunk_forward.argtypes + [P, ctypes.c_int32]
     lib.gdn_chunk_forward_profiled.restype = ctypes.c_int
+    lib.gdn_replay_forward_workspace_size.argtypes = [SP, P, P, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gdn_replay_forward_workspace_size.restype = ctypes.c_int
+    lib.gdn_replay_forward.argtypes = [SP, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.gdn_replay_forward.restype = ctypes.c_int
+    lib.gdn_replay_forward_profiled.argtypes = lib.gdn_replay_forward.argtypes + [P, ctypes.c_int32]
+    lib.gdn_replay_forward_profiled.restype = ctypes.c_int
+    lib.gdn_replay_forward_num_stages.argtypes = []
+    lib.gdn_replay_forward_num_stages.restype = ctypes.c_int32
+    lib.gdn_replay_forward_stage_name.argtypes = [ctypes.c_int32]
+    lib.gdn_replay_forward_stage_name.restype = ctypes.c_char_p
     lib.gdn_num_stages.argtypes = [ctypes.c_int32]
     lib.gdn_num_stages.restype = ctypes.c_int32
     lib.gdn_stage_name.argtypes = [ctypes.c_int32, ctypes.c_int32]
@@ -102,9 +112,17 @@ def stage_names(with_outputs: bool):
     return [lib.gdn_stage_name(int(with_outputs), i).decode() for i in range(n)]
 
 
-def _event_array(events, with_outputs):
+def replay_forward_stage_names():
+    """Names of the kernel stages ``replay_forward`` enqueues, in order."""
+    lib = load_library()
+    return [lib.gdn_replay_forward_stage_name(i).decode()
+            for i in range(lib.gdn_replay_forward_num_stages())]
+
+
+def _event_array(events, with_outputs, fused=False):
     """torch.cuda.Event list -> (void*[n], n) for the *_profiled entry points."""
-    n = load_library().gdn_num_stages(int(with_outputs)) + 1
+    lib = load_library()
+    n = (lib.gdn_replay_forward_num_stages() if fused else lib.gdn_num_stages(int(with_outputs))) + 1
     if len(events) != n:
         raise ValueError(f"need {n} events (one per stage boundary)")
     handles = []
@@ -299,3 +317,83 @@ def chunk_forward(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Te
         arr, n = _event_array(events, True)
         _check(lib.gdn_chunk_forward_profiled(*args, ctypes.cast(arr, ctypes.c_void_p), n))
     return o, state_out
+
+
+def replay_forward_workspace_size(num_seqs: int, num_k_heads: int, num_v_heads: int, d_k: int,
+                                  d_v: int, cu_tail_host: Sequence[int], cu_suf_host: Sequence[int],
+                                  dtype=torch.bfloat16) -> int:
+    lib = load_library()
+    ct = torch.tensor(list(cu_tail_host), dtype=torch.int32)
+    cs = torch.tensor(list(cu_suf_host), dtype=torch.int32)
+    shp = _shape(num_seqs, num_k_heads, num_v_heads, d_k, d_v,
+                 GDN_BF16 if dtype == torch.bfloat16 else GDN_F32, 1.0)
+    out = ctypes.c_size_t(0)
+    _check(lib.gdn_replay_forward_workspace_size(ctypes.byref(shp), _ptr(ct), _ptr(cs),
+                                                 ctypes.byref(out)))
+    return int(out.value)
+
+
+def replay_forward(k_tail: torch.Tensor, v_tail: torch.Tensor, g_tail: torch.Tensor,
+                   beta_tail: torch.Tensor, cu_tail, q: torch.Tensor, k: torch.Tensor,
+                   v: torch.Tensor, g: torch.Tensor, beta: torch.Tensor, cu_suf,
+                   cu_tail_host=None, cu_suf_host=None, scale: float = 1.0,
+                   state_mid: Optional[torch.Tensor] = None, o: Optional[torch.Tensor] = None,
+                   state_out: Optional[torch.Tensor] = None, write_state: bool = True,
+                   workspace: Optional[torch.Tensor] = None, events=None):
+    """Tail replay (paper Section 3, Eq. 2), then the forward over each
+    sequence's new suffix from the rebuilt state, in one call on torch's
+    current stream (same results as ``tail_replay`` then ``chunk_forward``).
+
+    Returns ``(o [Ts,Hv,d_v], state_mid [N,Hv,d_k,d_v], state_out or None)``.
+    """
+    lib = load_library()
+    device = q.device
+    dt = q.dtype
+    for name, t in (("k_tail", k_tail), ("v_tail", v_tail), ("q", q), ("k", k), ("v", v)):
+        _need(t, name, dt, device, 3)
+    Tt, hk, dk = k_tail.shape
+    Ts = q.shape[0]
+    hv, dv = v.shape[1], v.shape[2]
+    if tuple(v_tail.shape) != (Tt, hv, dv) or tuple(k.shape) != (Ts, hk, dk) or \
+            tuple(q.shape) != (Ts, hk, dk) or v.shape[0] != Ts:
+        raise ValueError("inconsistent tail/suffix shapes")
+    for name, t, T in (("g_tail", g_tail, Tt), ("beta_tail", beta_tail, Tt), ("g", g, Ts),
+                       ("beta", beta, Ts)):
+        _need(t, name, torch.float32, device, 2)
+        if tuple(t.shape) != (T, hv):
+            raise ValueError(f"{name} must be [T, Hv]")
+    cu_t, cu_t_host = _seqlens(cu_tail, cu_tail_host, device)
+    cu_s, cu_s_host = _seqlens(cu_suf, cu_suf_host, device)
+    n = cu_t_host.numel() - 1
+    if cu_s_host.numel() - 1 != n:
+        raise ValueError("tail and suffix must pack the same number of sequences")
+    if state_mid is None:
+        state_mid = torch.empty((n, hv, dk, dv), dtype=torch.float32, device=device)
+    if o is None:
+        o = torch.empty((Ts, hv, dv), dtype=dt, device=device)
+    if write_state and state_out is None:
+        state_out = torch.empty((n, hv, dk, dv), dtype=torch.float32, device=device)
+    for name, t in (("state_mid", state_mid), ("state_out", state_out)):
+        if t is not None:
+            _need(t, name, torch.float32, device, 4)
+            if tuple(t.shape) != (n, hv, dk, dv):
+                raise ValueError(f"{name} must be [N, Hv, d_k, d_v]")
+    _need(o, "o", dt, device, 3)
+    if tuple(o.shape) != (Ts, hv, dv):
+        raise ValueError("o must be [Ts, Hv, d_v]")
+    shp = _shape(n, hk, hv, dk, dv, _dtype_code(q), scale)
+    stream = torch.cuda.current_stream(device)
+    need = ctypes.c_size_t(0)
+    _check(lib.gdn_replay_forward_workspace_size(ctypes.byref(shp), _ptr(cu_t_host), _ptr(cu_s_host),
+                                                 ctypes.byref(need)))
+    ws = workspace if workspace is not None else _workspace(need.value, device, stream)
+    args = [ctypes.byref(shp), _ptr(cu_t_host), _ptr(cu_t), _ptr(k_tail), _ptr(v_tail),
+            _ptr(g_tail), _ptr(beta_tail), _ptr(cu_s_host), _ptr(cu_s), _ptr(q), _ptr(k), _ptr(v),
+            _ptr(g), _ptr(beta), _ptr(state_mid), _ptr(o), _ptr(state_out), _ptr(ws),
+            ws.numel() * ws.element_size(), ctypes.c_void_p(stream.cuda_stream)]
+    if events is None:
+        _check(lib.gdn_replay_forward(*args))
+    else:
+        arr, ne = _event_array(events, True, fused=True)
+        _check(lib.gdn_replay_forward_profiled(*args, ctypes.cast(arr, ctypes.c_void_p), ne))
+    return o, state_mid, state_out

@@ -85,45 +85,67 @@ gdn_status mark_all(const Args& a) {
   return GDN_OK;
 }
 
-template <typename TIn, int DK, int DV, bool FWD>
-gdn_status run(const Args& a) {
-  const gdn_shape& s = *a.s;
-  const Plan& p = *a.p;
-  u32x4* Kw = reinterpret_cast<u32x4*>(a.ws + p.off_K);
-  u32x4* Tw = reinterpret_cast<u32x4*>(a.ws + p.off_T);
-  float* Sw = reinterpret_cast<float*>(a.ws + p.off_S);
-  u32x4* Pw = FWD ? reinterpret_cast<u32x4*>(a.ws + p.off_P) : nullptr;
+template <typename TIn, int DK, bool FWD>
+gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, const void* q, const void* k,
+                        const float* g, const float* beta, char* ws, hipStream_t stream) {
+  if (p.num_slots == 0) return GDN_OK;
+  hipLaunchKernelGGL((k_intra<TIn, DK, FWD>), dim3(static_cast<uint32_t>(p.num_slots), s.num_v_heads),
+                     dim3(kThreads), 0, stream, cu, s.num_seqs, s.num_k_heads, s.num_v_heads,
+                     static_cast<const TIn*>(q), static_cast<const TIn*>(k), g, beta, s.scale,
+                     reinterpret_cast<u32x4*>(ws + p.off_K), reinterpret_cast<u32x4*>(ws + p.off_T),
+                     reinterpret_cast<float*>(ws + p.off_S),
+                     FWD ? reinterpret_cast<u32x4*>(ws + p.off_P) : nullptr);
+  return check_launch("intra launch");
+}
 
-  gdn_status st = mark(a, 0);
-  if (st != GDN_OK) return st;
-  if (p.num_slots > 0) {
-    hipLaunchKernelGGL((k_intra<TIn, DK, FWD>),
-                       dim3(static_cast<uint32_t>(p.num_slots), s.num_v_heads), dim3(kThreads), 0,
-                       a.stream, a.cu, s.num_seqs, s.num_k_heads, s.num_v_heads,
-                       static_cast<const TIn*>(a.q), static_cast<const TIn*>(a.k), a.g, a.beta,
-                       s.scale, Kw, Tw, Sw, Pw);
-    if ((st = check_launch("intra launch")) != GDN_OK) return st;
-  }
-  if ((st = mark(a, 1)) != GDN_OK) return st;
-  // The column-split kernel has the shortest chunk latency but one workgroup
-  // per CU; use it when its grid fits on the chip at once, else the whole-head
-  // kernel (4x the columns per CU, two waves per SIMD).
+// The column-split scan has the shortest chunk latency but one workgroup per
+// CU; it is used when its grid fits on the chip at once, else the whole-head
+// scan (4x the columns per CU, two waves per SIMD).
+gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return fail(GDN_ERR_HIP, "querying the device");
-  const uint32_t heads = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads;
-  const uint32_t col_groups = heads * (s.d_v / kColsPerGroup);
-  if (col_groups <= static_cast<uint32_t>(cus)) {
-    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(kColsThreads), 0, a.stream,
-                       a.cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v), Kw, Tw, Sw,
-                       Pw, a.state_in, static_cast<TIn*>(a.o), a.state_out);
+  *col_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kColsPerGroup);
+  *fits = *col_groups <= static_cast<uint32_t>(cus);
+  return GDN_OK;
+}
+
+template <typename TIn, int DK, int DV, bool FWD>
+gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, const void* v,
+                       const float* state_in, void* o, float* state_out, char* ws, hipStream_t stream) {
+  const u32x4* Kw = reinterpret_cast<const u32x4*>(ws + p.off_K);
+  const u32x4* Tw = reinterpret_cast<const u32x4*>(ws + p.off_T);
+  const float* Sw = reinterpret_cast<const float*>(ws + p.off_S);
+  const u32x4* Pw = FWD ? reinterpret_cast<const u32x4*>(ws + p.off_P) : nullptr;
+  bool fits = false;
+  uint32_t col_groups = 0;
+  gdn_status st = cols_fit(s, &fits, &col_groups);
+  if (st != GDN_OK) return st;
+  if (fits) {
+    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(kColsThreads), 0, stream, cu,
+                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, Pw,
+                       state_in, static_cast<TIn*>(o), state_out);
   } else {
-    hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(heads), dim3(head_threads(DV)), 0, a.stream,
-                       a.cu, s.num_k_heads, s.num_v_heads, static_cast<const TIn*>(a.v), Kw, Tw, Sw, Pw,
-                       a.state_in, static_cast<TIn*>(a.o), a.state_out);
+    hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
+                       dim3(head_threads(DV)), 0, stream, cu, s.num_k_heads, s.num_v_heads,
+                       static_cast<const TIn*>(v), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o),
+                       state_out);
   }
-  if ((st = check_launch("scan launch")) != GDN_OK) return st;
+  return check_launch("scan launch");
+}
+
+template <typename TIn, int DK, int DV, bool FWD>
+gdn_status run(const Args& a) {
+  const gdn_shape& s = *a.s;
+  gdn_status st = mark(a, 0);
+  if (st != GDN_OK) return st;
+  if ((st = launch_intra<TIn, DK, FWD>(s, *a.p, a.cu, a.q, a.k, a.g, a.beta, a.ws, a.stream)) != GDN_OK)
+    return st;
+  if ((st = mark(a, 1)) != GDN_OK) return st;
+  if ((st = launch_scan<TIn, DK, DV, FWD>(s, *a.p, a.cu, a.v, a.state_in, a.o, a.state_out, a.ws, a.stream)) !=
+      GDN_OK)
+    return st;
   return mark(a, 2);
 }
 
@@ -237,6 +259,142 @@ gdn_status chunk_forward_impl(const gdn_shape* shape, const int32_t* cu_seqlens_
   return gdn::dispatch<true>(a);
 }
 
+// ---------------------------------------------------------------- replay then forward
+constexpr int32_t kNumFusedStages = 3;
+const char* const kFusedStageNames[kNumFusedStages] = {"tail intra", "tail scan + suffix intra",
+                                                       "suffix scan"};
+
+struct FusedArgs {
+  const gdn_shape* s;
+  const Plan* pt;      // tail plan (no outputs)
+  const Plan* ps;      // suffix plan (outputs)
+  const int32_t* cu_t;
+  const void* k_t;
+  const void* v_t;
+  const float* g_t;
+  const float* beta_t;
+  const int32_t* cu_s;
+  const void* q;
+  const void* k;
+  const void* v;
+  const float* g;
+  const float* beta;
+  float* state_mid;
+  void* o;
+  float* state_out;
+  char* ws_t;
+  char* ws_s;
+  hipStream_t stream;
+  void* const* events;   // NULL, or kNumFusedStages + 1 events
+};
+
+gdn_status fmark(const FusedArgs& a, int stage) {
+  if (!a.events) return GDN_OK;
+  const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(a.events[stage]), a.stream);
+  if (e != hipSuccess) return fail(GDN_ERR_HIP, std::string("hipEventRecord: ") + hipGetErrorString(e));
+  return GDN_OK;
+}
+
+template <typename TIn, int DK, int DV>
+gdn_status run_fused(const FusedArgs& a) {
+  const gdn_shape& s = *a.s;
+  const Plan& pt = *a.pt;
+  const Plan& ps = *a.ps;
+  gdn_status st = fmark(a, 0);
+  if (st != GDN_OK) return st;
+  if ((st = launch_intra<TIn, DK, false>(s, pt, a.cu_t, nullptr, a.k_t, a.g_t, a.beta_t, a.ws_t, a.stream)) !=
+      GDN_OK)
+    return st;
+  if ((st = fmark(a, 1)) != GDN_OK) return st;
+  bool fits = false;
+  uint32_t n_scan = 0;
+  if ((st = cols_fit(s, &fits, &n_scan)) != GDN_OK) return st;
+  if (fits && ps.num_slots > 0) {
+    // the suffix's records are built on the CUs the tail replay leaves idle
+    const uint32_t blocks = n_scan + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
+    hipLaunchKernelGGL((k_scan_cols_intra<TIn, DK>), dim3(blocks), dim3(4 * kWave), 0, a.stream,
+                       static_cast<int32_t>(n_scan), a.cu_t, s.num_k_heads, s.num_v_heads, s.d_v,
+                       static_cast<const TIn*>(a.v_t), reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
+                       reinterpret_cast<const u32x4*>(a.ws_t + pt.off_T),
+                       reinterpret_cast<const float*>(a.ws_t + pt.off_S), a.state_mid,
+                       static_cast<int32_t>(ps.num_slots), a.cu_s, s.num_seqs, static_cast<const TIn*>(a.q),
+                       static_cast<const TIn*>(a.k), a.g, a.beta, s.scale,
+                       reinterpret_cast<u32x4*>(a.ws_s + ps.off_K), reinterpret_cast<u32x4*>(a.ws_s + ps.off_T),
+                       reinterpret_cast<float*>(a.ws_s + ps.off_S), reinterpret_cast<u32x4*>(a.ws_s + ps.off_P));
+    if ((st = check_launch("tail scan + suffix intra launch")) != GDN_OK) return st;
+  } else {
+    if ((st = launch_scan<TIn, DK, DV, false>(s, pt, a.cu_t, a.v_t, nullptr, nullptr, a.state_mid, a.ws_t,
+                                              a.stream)) != GDN_OK)
+      return st;
+    if ((st = launch_intra<TIn, DK, true>(s, ps, a.cu_s, a.q, a.k, a.g, a.beta, a.ws_s, a.stream)) != GDN_OK)
+      return st;
+  }
+  if ((st = fmark(a, 2)) != GDN_OK) return st;
+  if ((st = launch_scan<TIn, DK, DV, true>(s, ps, a.cu_s, a.v, a.state_mid, a.o, a.state_out, a.ws_s,
+                                           a.stream)) != GDN_OK)
+    return st;
+  return fmark(a, 3);
+}
+
+template <int DK, int DV>
+gdn_status fused_dtype(const FusedArgs& a) {
+  return a.s->qkv_dtype == GDN_BF16 ? run_fused<uint16_t, DK, DV>(a) : run_fused<float, DK, DV>(a);
+}
+
+gdn_status fused_plans(const gdn_shape* shape, const int32_t* cu_tail_host, const int32_t* cu_suf_host,
+                       Plan* pt, Plan* ps, size_t* off_s, size_t* bytes) {
+  std::string err;
+  gdn_status st = make_plan(shape, cu_tail_host, false, pt, &err);
+  if (st != GDN_OK) return fail(st, "tail: " + err);
+  if ((st = make_plan(shape, cu_suf_host, true, ps, &err)) != GDN_OK) return fail(st, "suffix: " + err);
+  *off_s = (pt->bytes + kAlign - 1) / kAlign * kAlign;
+  *bytes = *off_s + ps->bytes;
+  return GDN_OK;
+}
+
+gdn_status replay_forward_impl(const gdn_shape* shape, const int32_t* cu_tail_host, const int32_t* cu_tail,
+                               const void* k_tail, const void* v_tail, const float* g_tail,
+                               const float* beta_tail, const int32_t* cu_suf_host, const int32_t* cu_suf,
+                               const void* q, const void* k, const void* v, const float* g,
+                               const float* beta, float* state_mid, void* o, float* state_out,
+                               void* workspace, size_t workspace_bytes, void* stream, void* const* events) {
+  Plan pt, ps;
+  size_t off_s = 0, bytes = 0;
+  gdn_status st = fused_plans(shape, cu_tail_host, cu_suf_host, &pt, &ps, &off_s, &bytes);
+  if (st != GDN_OK) return st;
+  if (shape->num_seqs > 0 && (!cu_tail || !cu_suf)) return fail(GDN_ERR_NULL_ARG, "cu_seqlens (device) is NULL");
+  if (bytes > 0 && !workspace) return fail(GDN_ERR_WORKSPACE, "workspace is NULL");
+  if (workspace_bytes < bytes)
+    return fail(GDN_ERR_WORKSPACE, "workspace too small: need " + std::to_string(bytes) + " bytes, got " +
+                                       std::to_string(workspace_bytes));
+  if (reinterpret_cast<uintptr_t>(workspace) % kAlign != 0)
+    return fail(GDN_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (shape->num_seqs > 0 && !state_mid) return fail(GDN_ERR_NULL_ARG, "state_mid is NULL");
+  if (pt.total_tokens > 0 && (!k_tail || !v_tail || !g_tail || !beta_tail))
+    return fail(GDN_ERR_NULL_ARG, "k_tail, v_tail, g_tail and beta_tail must be non-NULL");
+  if (ps.total_tokens > 0 && (!q || !k || !v || !g || !beta || !o))
+    return fail(GDN_ERR_NULL_ARG, "q, k, v, g, beta and o must be non-NULL");
+  for (const void* ptr : {k_tail, v_tail, q, k, v, static_cast<const void*>(o)})
+    if (reinterpret_cast<uintptr_t>(ptr) % 16 != 0)
+      return fail(GDN_ERR_UNSUPPORTED, "k_tail, v_tail, q, k, v and o must be 16-byte aligned");
+  if (state_out && state_out != state_mid) {
+    const size_t n = static_cast<size_t>(shape->num_seqs) * shape->num_v_heads * shape->d_k * shape->d_v;
+    if (state_mid < state_out + n && state_out < state_mid + n)
+      return fail(GDN_ERR_BAD_SHAPE, "state_out overlaps state_mid without being equal");
+  }
+  const FusedArgs a{shape, &pt, &ps, cu_tail, k_tail, v_tail, g_tail, beta_tail, cu_suf, q, k, v, g, beta,
+                    state_mid, o, state_out, static_cast<char*>(workspace),
+                    static_cast<char*>(workspace) + off_s, static_cast<hipStream_t>(stream), events};
+  if (shape->num_seqs == 0) {
+    for (int i = 0; i <= kNumFusedStages; ++i)
+      if ((st = fmark(a, i)) != GDN_OK) return st;
+    return GDN_OK;
+  }
+  const int dk = shape->d_k, dv = shape->d_v;
+  if (dk == 64) return dv == 64 ? fused_dtype<64, 64>(a) : fused_dtype<64, 128>(a);
+  return dv == 64 ? fused_dtype<128, 64>(a) : fused_dtype<128, 128>(a);
+}
+
 }  // namespace
 }  // namespace gdn
 
@@ -282,6 +440,49 @@ gdn_status gdn_chunk_forward_profiled(const gdn_shape* shape, const int32_t* cu_
   return gdn::chunk_forward_impl(shape, cu_seqlens_host, cu_seqlens, q, k, v, g, beta,
                                  state_in, o, state_out, workspace, workspace_bytes, stream,
                                  stage_events);
+}
+
+gdn_status gdn_replay_forward_workspace_size(const gdn_shape* shape, const int32_t* cu_tail_host,
+                                             const int32_t* cu_suf_host, size_t* bytes) {
+  if (!bytes) return gdn::fail(GDN_ERR_NULL_ARG, "bytes is NULL");
+  gdn::Plan pt, ps;
+  size_t off_s = 0;
+  return gdn::fused_plans(shape, cu_tail_host, cu_suf_host, &pt, &ps, &off_s, bytes);
+}
+
+gdn_status gdn_replay_forward(const gdn_shape* shape, const int32_t* cu_tail_host, const int32_t* cu_tail,
+                              const void* k_tail, const void* v_tail, const float* g_tail,
+                              const float* beta_tail, const int32_t* cu_suf_host, const int32_t* cu_suf,
+                              const void* q, const void* k, const void* v, const float* g, const float* beta,
+                              float* state_mid, void* o, float* state_out, void* workspace,
+                              size_t workspace_bytes, void* stream) {
+  return gdn::replay_forward_impl(shape, cu_tail_host, cu_tail, k_tail, v_tail, g_tail, beta_tail, cu_suf_host,
+                                  cu_suf, q, k, v, g, beta, state_mid, o, state_out, workspace, workspace_bytes,
+                                  stream, nullptr);
+}
+
+gdn_status gdn_replay_forward_profiled(const gdn_shape* shape, const int32_t* cu_tail_host,
+                                       const int32_t* cu_tail, const void* k_tail, const void* v_tail,
+                                       const float* g_tail, const float* beta_tail, const int32_t* cu_suf_host,
+                                       const int32_t* cu_suf, const void* q, const void* k, const void* v,
+                                       const float* g, const float* beta, float* state_mid, void* o,
+                                       float* state_out, void* workspace, size_t workspace_bytes, void* stream,
+                                       void* const* stage_events, int32_t num_events) {
+  if (!stage_events) return gdn::fail(GDN_ERR_NULL_ARG, "stage_events is NULL");
+  if (num_events != gdn::kNumFusedStages + 1)
+    return gdn::fail(GDN_ERR_BAD_SHAPE, "num_events must be gdn_replay_forward_num_stages() + 1");
+  for (int i = 0; i < num_events; ++i)
+    if (!stage_events[i]) return gdn::fail(GDN_ERR_NULL_ARG, "a stage event is NULL");
+  return gdn::replay_forward_impl(shape, cu_tail_host, cu_tail, k_tail, v_tail, g_tail, beta_tail, cu_suf_host,
+                                  cu_suf, q, k, v, g, beta, state_mid, o, state_out, workspace, workspace_bytes,
+                                  stream, stage_events);
+}
+
+int32_t gdn_replay_forward_num_stages(void) { return gdn::kNumFusedStages; }
+
+const char* gdn_replay_forward_stage_name(int32_t stage) {
+  if (stage < 0 || stage >= gdn::kNumFusedStages) return "";
+  return gdn::kFusedStageNames[stage];
 }
 
 int32_t gdn_num_stages(int32_t with_outputs) {

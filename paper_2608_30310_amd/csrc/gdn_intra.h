@@ -55,40 +55,59 @@ __device__ __forceinline__ f32x4 mma_f32(float a, float b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
 }
 
-// grid = (num_slots, Hv): one workgroup per (chunk slot, value head).
+// LDS of one intra workgroup.
 template <typename TIn, int DK, bool FWD>
-__global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, int32_t num_seqs,
-                                               int32_t hk, int32_t hv,
-                                               const TIn* __restrict__ q,
-                                               const TIn* __restrict__ k,
-                                               const float* __restrict__ g,
-                                               const float* __restrict__ beta, float scale,
-                                               u32x4* __restrict__ Kw,
-                                               u32x4* __restrict__ Tw,
-                                               float* __restrict__ Sw,
-                                               u32x4* __restrict__ Pw) {
-  constexpr bool SPLIT = sizeof(TIn) == 4;   // fp32 inputs are not exact bf16
-  constexpr int KP = DK + 8;                 // padded LDS row (bf16 elements)
-  constexpr int NL = SPLIT ? 2 : 1;          // hi (and lo) copies
-  constexpr int AP = kChunk + 4;             // fp32 row pitch of A, T and P
+struct IntraLds {
+  static constexpr bool kSplit = sizeof(TIn) == 4;
+  static constexpr int KP = DK + 8;                 // padded LDS row (bf16 elements)
+  static constexpr int NL = kSplit ? 2 : 1;         // hi (and lo) copies
+  static constexpr int AP = kChunk + 4;             // fp32 row pitch of A, T and P
+  alignas(16) uint16_t Ks[NL][kChunk][KP];
+  alignas(16) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
+  alignas(16) float As[kChunk][AP];                 // A (strictly lower)
+  alignas(16) float Ts[kChunk][AP];                 // T = (I + A)^-1
+  alignas(16) float Ps[FWD ? kChunk : 1][AP];
+  alignas(16) float Ys[4][16][17];                  // per-wave block scratch
+  alignas(16) float Gs[kChunk];
+  alignas(16) float Bs[kChunk];
+};
+
+// One intra workgroup (256 threads) for chunk slot `slot` and value head `h`,
+// with its LDS in `sm`.
+template <typename TIn, int DK, bool FWD>
+__device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot, int h,
+                                           const int32_t* __restrict__ cu, int32_t num_seqs,
+                                           int32_t hk, int32_t hv,
+                                           const TIn* __restrict__ q,
+                                           const TIn* __restrict__ k,
+                                           const float* __restrict__ g,
+                                           const float* __restrict__ beta, float scale,
+                                           u32x4* __restrict__ Kw,
+                                           u32x4* __restrict__ Tw,
+                                           float* __restrict__ Sw,
+                                           u32x4* __restrict__ Pw) {
+  using S = IntraLds<TIn, DK, FWD>;
+  constexpr bool SPLIT = S::kSplit;
+  constexpr int KP = S::KP;
+  constexpr int NL = S::NL;
+  constexpr int AP = S::AP;
   constexpr int NK = DK / 32;
   constexpr int NKA = ka_frags(DK), NKT = kt_frags(DK);
   constexpr int NKF = k_record_frags(DK, FWD);   // fragments per bf16 part
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[NL][kChunk][KP];
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
-  __shared__ __attribute__((aligned(16))) float As[kChunk][AP];   // A (strictly lower)
-  __shared__ __attribute__((aligned(16))) float Ts[kChunk][AP];   // T = (I + A)^-1
-  __shared__ __attribute__((aligned(16))) float Ps[FWD ? kChunk : 1][AP];
-  __shared__ __attribute__((aligned(16))) float Ys[4][16][17];    // per-wave block scratch
-  __shared__ __attribute__((aligned(16))) float Gs[kChunk];
-  __shared__ __attribute__((aligned(16))) float Bs[kChunk];
+  auto& Ks = sm.Ks;
+  auto& Qs = sm.Qs;
+  auto& As = sm.As;
+  auto& Ts = sm.Ts;
+  auto& Ps = sm.Ps;
+  auto& Ys = sm.Ys;
+  auto& Gs = sm.Gs;
+  auto& Bs = sm.Bs;
+  (void)KP;
 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave;
   const int lg = lane / 16, lr = lane % 16;
-  const int slot = blockIdx.x;
-  const int h = blockIdx.y;
   const int grp = hv / hk;
   const int kh = h / grp;
   const int64_t rec = static_cast<int64_t>(slot) * hv + h;
@@ -366,6 +385,23 @@ __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, i
     sc[3 * kChunk + tid] = scale * __expf(Gs[tid]);
     sc[4 * kChunk + tid] = __expf(gl);
   }
+}
+
+// grid = (num_slots, Hv): one workgroup per (chunk slot, value head).
+template <typename TIn, int DK, bool FWD>
+__global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, int32_t num_seqs,
+                                               int32_t hk, int32_t hv,
+                                               const TIn* __restrict__ q,
+                                               const TIn* __restrict__ k,
+                                               const float* __restrict__ g,
+                                               const float* __restrict__ beta, float scale,
+                                               u32x4* __restrict__ Kw,
+                                               u32x4* __restrict__ Tw,
+                                               float* __restrict__ Sw,
+                                               u32x4* __restrict__ Pw) {
+  __shared__ IntraLds<TIn, DK, FWD> sm;
+  intra_body<TIn, DK, FWD>(sm, blockIdx.x, blockIdx.y, cu, num_seqs, hk, hv, q, k, g, beta, scale, Kw, Tw,
+                           Sw, Pw);
 }
 
 }  // namespace gdn

@@ -32,9 +32,10 @@ namespace gdn {
 constexpr int kLdsBytes = 160 * 1024;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(3))) unsigned char lds_byte;   // LDS bytes
 
 // 16 bytes per lane from `src` (per lane) to LDS `dst + 16 * lane` (dst uniform).
-__device__ __forceinline__ void dma16(const void* src, void* dst) {
+__device__ __forceinline__ void dma16(const void* src, lds_byte* dst) {
   __builtin_amdgcn_global_load_lds(src, (lds_ptr_t)dst, 16, 0, 0);
 }
 
@@ -52,7 +53,7 @@ __device__ __forceinline__ int swz(int row, int byte_in_row) {
 // `blk` of the tile) into a swizzled LDS row tile; rows past `rows` repeat the
 // last valid row.
 template <int ROW_BYTES, typename T>
-__device__ __forceinline__ void dma_rows(const T* row0, int64_t row_stride, int rows, unsigned char* dst,
+__device__ __forceinline__ void dma_rows(const T* row0, int64_t row_stride, int rows, lds_byte* dst,
                                          int blk, int lane) {
   constexpr int pieces = ROW_BYTES / 16;
   constexpr int rows_per_block = 1024 / ROW_BYTES;
@@ -123,7 +124,7 @@ struct ChunkSrc {
 
 // DMA job j of a chunk (0 <= j < L::kJobs) into LDS buffer `base`.
 template <typename L, typename TIn>
-__device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, unsigned char* base, int j, int lane) {
+__device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, lds_byte* base, int j, int lane) {
   if (j < L::kKJobs) {
     dma16(c.krec + 1024 * j + 16 * lane, base + L::kOffK + 1024 * j);
   } else if (j < L::kKJobs + L::kTJobs) {
@@ -430,23 +431,31 @@ constexpr int kColsPerGroup = 32;
 constexpr int kColsThreads = 3 * kWave;
 
 template <typename TIn, int DK, bool FWD>
-__global__ __launch_bounds__(kColsThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
-                 const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
-                 const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
-                 const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
-  using L = ScanLds<TIn, DK, kColsPerGroup, FWD, true>;
+using ColsLds = ScanLds<TIn, DK, kColsPerGroup, FWD, true>;
+
+// One column-split workgroup (block `block` of `nblocks`), LDS in `lds`.
+// Waves 0 and 1 compute, wave 2 issues the DMA; any further waves of the
+// workgroup only take part in the barriers.
+template <typename TIn, int DK, bool FWD>
+__device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int nblocks,
+                                               const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
+                                               int32_t dv, const TIn* __restrict__ v,
+                                               const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                                               const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
+                                               const float* __restrict__ state_in, TIn* __restrict__ o,
+                                               float* __restrict__ state_out) {
+  using L = ColsLds<TIn, DK, FWD>;
   constexpr int NT = DK / 16;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
   const int tid = threadIdx.x;
   // wave index made provably uniform: DMA destinations (M0) stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const bool data_wave = wave == 2;
+  const bool data_wave = wave >= 2;
+  const bool dma_wave = wave == 2;
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
   const int ngroups = dv / kColsPerGroup;
   // logical unit: the column groups of a value head, then the value heads of a
   // key head, are adjacent (same XCD, shared records in its L2)
-  const int unit = xcd_remap(blockIdx.x, gridDim.x);
+  const int unit = xcd_remap(block, nblocks);
   const int col0 = kColsPerGroup * (unit % ngroups);
   const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
   const int col = col0 + 16 * wave + lr;
@@ -454,7 +463,7 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   auto dma_chunk = [&](int ci, int b) __attribute__((always_inline)) {
     const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
 #pragma unroll
-    for (int j = 0; j < L::kJobs; ++j) dma_job<L, TIn>(c, vrow, lds + b * L::kBytes, j, lane);
+    for (int j = 0; j < L::kJobs; ++j) dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
   };
 
   f32x4 M[NT];
@@ -463,7 +472,7 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * dv + col;
   if (!data_wave) load_state<DK>(state_in, sbase, dv, lg, M, mb);
 
-  if (data_wave && u.nch > 0) {
+  if (dma_wave && u.nch > 0) {
     dma_chunk(0, 0);
     wait_dma();
   }
@@ -471,7 +480,7 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   for (int ci = 0; ci < u.nch; ++ci) {
     const int b = L::kBuffers == 2 ? (ci & 1) : 0;
     if (data_wave) {
-      if (L::kBuffers == 2 && ci + 1 < u.nch) {
+      if (dma_wave && L::kBuffers == 2 && ci + 1 < u.nch) {
         dma_chunk(ci + 1, b ^ 1);   // lands while the compute waves work on buffer b
         wait_dma();
       }
@@ -480,11 +489,12 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
         if (ci > 0) store_chunk_out(o, u, ci - 1, hv, dv, col - lr, lane, pout);
       }
       const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
-      chunk_step<L, DK, FWD>(lds + b * L::kBytes, 16 * wave, pg, lane, M, mb, pout, [](int) {});
+      chunk_step<L, DK, FWD>((const unsigned char*)(lds_l + b * L::kBytes), 16 * wave, pg, lane, M, mb, pout,
+                             [](int) {});
     }
     if (L::kBuffers == 1) {
       __syncthreads();   // the compute waves are done with the only buffer
-      if (data_wave && ci + 1 < u.nch) {
+      if (dma_wave && ci + 1 < u.nch) {
         dma_chunk(ci + 1, 0);
         wait_dma();
       }
@@ -505,6 +515,50 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   }
 }
 
+template <typename TIn, int DK, bool FWD>
+__global__ __launch_bounds__(kColsThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
+                 const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                 const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
+                 const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
+  using L = ColsLds<TIn, DK, FWD>;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+  scan_cols_body<TIn, DK, FWD>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw, Sw, Pw,
+                               state_in, o, state_out);
+}
+
+// ---------------------------------------------------------------- replay scan + suffix intra
+// One launch, two kinds of workgroup (256 threads): blocks [0, n_scan) run the
+// column-split tail replay (FWD = false, zero start, final state to
+// `state_mid`; the fourth wave only takes part in the barriers), the rest run
+// k_intra for the suffix chunks (with outputs), so the suffix's records are
+// built on the CUs the replay leaves idle.  No workgroup waits for another.
+template <typename TIn, int DK>
+__global__ __launch_bounds__(4 * kWave) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_scan_cols_intra(int32_t n_scan, const int32_t* __restrict__ cu_t, int32_t hk, int32_t hv, int32_t dv,
+                       const TIn* __restrict__ v_t, const u32x4* __restrict__ Kw_t,
+                       const u32x4* __restrict__ Tw_t, const float* __restrict__ Sw_t,
+                       float* __restrict__ state_mid,
+                       int32_t slots_s, const int32_t* __restrict__ cu_s, int32_t num_seqs,
+                       const TIn* __restrict__ q_s, const TIn* __restrict__ k_s,
+                       const float* __restrict__ g_s, const float* __restrict__ beta_s, float scale,
+                       u32x4* __restrict__ Kw_s, u32x4* __restrict__ Tw_s, float* __restrict__ Sw_s,
+                       u32x4* __restrict__ Pw_s) {
+  using LS = ColsLds<TIn, DK, false>;
+  using LI = IntraLds<TIn, DK, true>;
+  constexpr size_t kScanBytes = static_cast<size_t>(LS::kBuffers) * LS::kBytes;
+  constexpr size_t kBytes = kScanBytes > sizeof(LI) ? kScanBytes : sizeof(LI);
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kBytes];
+  if (static_cast<int>(blockIdx.x) < n_scan) {
+    scan_cols_body<TIn, DK, false>((lds_byte*)smem, blockIdx.x, n_scan, cu_t, hk, hv, dv, v_t, Kw_t, Tw_t,
+                                   Sw_t, nullptr, nullptr, nullptr, state_mid);
+  } else {
+    const int i = blockIdx.x - n_scan;
+    intra_body<TIn, DK, true>(*reinterpret_cast<LI*>(smem), i % slots_s, i / slots_s, cu_s, num_seqs, hk, hv,
+                              q_s, k_s, g_s, beta_s, scale, Kw_s, Tw_s, Sw_s, Pw_s);
+  }
+}
+
 // ---------------------------------------------------------------- throughput kernel
 // grid = N x Hv: d_v/16 waves (two per SIMD for d_v = 128), each 16 columns,
 // sharing one copy of the chunk's records per head; every wave issues an equal
@@ -522,7 +576,8 @@ void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
   constexpr int NT = DK / 16;
   constexpr int W = DV / 16;
   constexpr int PER_WAVE = (L::kJobs + W - 1) / W;   // DMA jobs per wave per chunk
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+  __shared__ __attribute__((aligned(1024))) unsigned char lds_g[L::kBuffers * L::kBytes];
+  lds_byte* lds = (lds_byte*)lds_g;
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
@@ -566,7 +621,7 @@ void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
       }
     };
     const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
-    chunk_step<L, DK, FWD>(lds + b * L::kBytes, 16 * wave, pg, lane, M, mb, pout, hook);
+    chunk_step<L, DK, FWD>((const unsigned char*)(lds + b * L::kBytes), 16 * wave, pg, lane, M, mb, pout, hook);
     if (L::kBuffers == 1) {
       __syncthreads();   // every wave is done with the only buffer
       if (ci + 1 < u.nch) dma_share(ci + 1, 0, 0, PER_WAVE);

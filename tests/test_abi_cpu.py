@@ -31,6 +31,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("gdn_tail_replay", "gdn_chunk_forward", "gdn_workspace_size",
+                 "gdn_replay_forward", "gdn_replay_forward_workspace_size",
                  "gdn_replay_len", "gdn_status_string", "gdn_last_error"):
         assert want in names
 
@@ -174,3 +175,46 @@ def test_replay_len_matches_the_oracle():
 def test_binding_raises_gdn_error():
     with pytest.raises(gdn.GDNError):
         binding._check(2)
+
+
+def test_replay_forward_workspace_is_both_plans():
+    # the fused call holds the tail plan (256-byte aligned) then the suffix plan
+    lib = gdn.load_library()
+    shape = _shape(num_seqs=2)
+    ct, cs = [0, 819, 1230], [0, 512, 600]
+    _, nt = _ws_size(shape, _cu(ct), 0)
+    _, ns = _ws_size(shape, _cu(cs), 1)
+    out = ctypes.c_size_t(0)
+    st = lib.gdn_replay_forward_workspace_size(ctypes.byref(shape), ctypes.cast(_cu(ct), ctypes.c_void_p),
+                                               ctypes.cast(_cu(cs), ctypes.c_void_p), ctypes.byref(out))
+    assert st == 0 and out.value == (nt + 255) // 256 * 256 + ns
+    assert gdn.replay_forward_workspace_size(2, 16, 32, 128, 128, ct, cs) == out.value
+    assert gdn.replay_forward_stage_names() == ["tail intra", "tail scan + suffix intra", "suffix scan"]
+    # sequence counts must agree
+    st = lib.gdn_replay_forward_workspace_size(ctypes.byref(_shape(num_seqs=2)),
+                                               ctypes.cast(_cu(ct), ctypes.c_void_p),
+                                               ctypes.cast(_cu([0, 5, 3]), ctypes.c_void_p),
+                                               ctypes.byref(out))
+    assert st == 3
+
+
+@needs_no_gpu
+@pytest.mark.parametrize("case", ["null_mid", "null_o", "misaligned_k_tail", "small_ws", "overlap"])
+def test_replay_forward_rejects_before_launch(case):
+    lib = gdn.load_library()
+    shape = _shape(num_seqs=1)
+    ct, cs = _cu([0, 100]), _cu([0, 50])
+    out = ctypes.c_size_t(0)
+    assert lib.gdn_replay_forward_workspace_size(ctypes.byref(shape), ctypes.cast(ct, ctypes.c_void_p),
+                                                 ctypes.cast(cs, ctypes.c_void_p), ctypes.byref(out)) == 0
+    n_state = 32 * 128 * 128 * 4
+    mid = ctypes.c_void_p(0x100000)
+    fin = ctypes.c_void_p(0x100000 + (n_state // 2 if case == "overlap" else 2 * n_state))
+    kt = ctypes.c_void_p(0x1008) if case == "misaligned_k_tail" else FAKE
+    st = lib.gdn_replay_forward(ctypes.byref(shape), ctypes.cast(ct, ctypes.c_void_p), FAKE, kt, FAKE,
+                                FAKE, FAKE, ctypes.cast(cs, ctypes.c_void_p), FAKE, FAKE, FAKE, FAKE,
+                                FAKE, FAKE, None if case == "null_mid" else mid,
+                                None if case == "null_o" else FAKE, fin, ctypes.c_void_p(0x20000),
+                                out.value - (256 if case == "small_ws" else 0), None)
+    want = {"null_mid": 1, "null_o": 1, "misaligned_k_tail": 4, "small_ws": 5, "overlap": 2}[case]
+    assert st == want, lib.gdn_last_error().decode()

@@ -187,3 +187,29 @@ def test_whole_head_and_column_kernels_agree():
         a, b = int(cu[i]), int(cu[i + 1])
         rel = (o[a:b].float() - oi.float()).norm() / oi.float().norm()
         assert rel.item() <= 1e-3   # bf16 outputs: one rounding step apart at most
+
+
+@pytest.mark.parametrize("case", ["one", "ragged", "wide"])
+def test_replay_forward_equals_the_two_calls_bitwise(case):
+    # the fused call runs the same kernels (the suffix's chunk preparation
+    # beside the tail scan), so it must reproduce tail_replay + chunk_forward
+    if case == "one":
+        rs, ss = [333], [200]
+    elif case == "ragged":
+        rs, ss = [0, 1, 64, 130, 257], [65, 0, 1, 200, 64]
+    else:   # enough heads that the whole-head scan kernel runs
+        rs = [1 + (37 * i) % 150 for i in range(72)]
+        ss = [1 + (53 * i) % 120 for i in range(72)]
+    tails = synth.pack([_seq(i, r, start=0) for i, r in enumerate(rs)])
+    sufs = synth.pack([_seq(i, s, start=r) for i, (r, s) in enumerate(zip(rs, ss))])
+    xt, xs = device_inputs(tails), device_inputs(sufs)
+    st = gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"])
+    o, st2 = gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"],
+                               xs["cu_host"], state_in=st, scale=0.7)
+    of, mid, stf = gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"],
+                                      xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"],
+                                      cu_tail_host=xt["cu_host"], cu_suf_host=xs["cu_host"],
+                                      scale=0.7)
+    assert torch.equal(mid, st)
+    assert torch.equal(of, o)
+    assert torch.equal(stf, st2)

@@ -101,6 +101,23 @@ def _chain(shape, hits, outputs_scale=1.0):
             output_err(to_f64(o), w_o, sufs.cu_seqlens))
 
 
+def test_workload1_fused_replay_forward():
+    # the bench configuration through the fused entry point, against the oracle
+    shape, hits = workloads.workload1(819)
+    tails = synth.pack([h.tail(shape) for h in hits])
+    sufs = synth.pack([h.suffix(shape) for h in hits])
+    xt, xs = device_inputs(tails), device_inputs(sufs)
+    o, mid, st = gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"],
+                                    xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"],
+                                    cu_tail_host=xt["cu_host"], cu_suf_host=xs["cu_host"])
+    _, w_tail = oracle_run(tails)
+    w_o, w_st = oracle_run(sufs, state_in=w_tail, outputs=True)
+    e = (state_err(to_f64(mid), w_tail), state_err(to_f64(st), w_st),
+         output_err(to_f64(o), w_o, sufs.cu_seqlens))
+    _report("workload1 fused r=819", tail=e[0], fwd_state=e[1], out=e[2])
+    assert e[0] <= STATE_TOL and e[1] <= STATE_TOL and e[2] <= OUTPUT_TOL
+
+
 def test_workload0_small_fp32():
     shape, hits = workloads.workload0()
     e = _chain(shape, hits)
