@@ -371,9 +371,15 @@ def main():
     # runs (the tail replay's or the suffix forward's)
     fused = {k: v for k, v in stages.items() if k.startswith("replay_forward.")}
     dom = max(fused, key=lambda k: fused[k]["mean_us"])
-    on_tail = dom in ("replay_forward.tail intra", "replay_forward.tail scan + suffix intra")
-    kbytes = tail_bytes if on_tail else fwd_bytes
-    kflops = tail_flops if on_tail else fwd_flops
+    grp = hv // hk
+    # the suffix's chunk preparation reads q, k (shared by the group), g and
+    # beta and forms K K^T and Q K^T per chunk
+    prep_bytes = s * hv * (2 * elt * dk / grp + 8)
+    prep_flops = s * hv * (2 * 2 * CHUNK * dk / grp)
+    kbytes, kflops = {"replay_forward.tail intra": (tail_bytes, tail_flops),
+                      "replay_forward.tail scan + suffix intra": (tail_bytes + prep_bytes,
+                                                                  tail_flops + prep_flops),
+                      "replay_forward.suffix scan": (fwd_bytes, fwd_flops)}[dom]
     dom_s = stages[dom]["mean_us"] * 1e-6
     achieved = kbytes / dom_s / 1e9
     kname = {"replay_forward.tail intra": "gdn::k_intra<unsigned short, 128, false>",
