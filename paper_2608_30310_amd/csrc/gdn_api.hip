@@ -34,7 +34,7 @@ thread_local std::string t_last_error;
 
 constexpr int kThreads = 256;
 // grid limits in make_plan assume <= 1024 work items per (sequence, head) in any grid dimension
-static_assert(kThreads <= 256 && kColsThreads <= 256 && head_threads(128) <= 1024, "grid limits");
+static_assert(kThreads <= 256 && cols_threads(true) <= 256 && head_threads(128) <= 1024, "grid limits");
 
 // ------------------------------------------------------------ host side
 gdn_status fail(gdn_status st, const std::string& msg) {
@@ -123,7 +123,7 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
   gdn_status st = cols_fit(s, &fits, &col_groups);
   if (st != GDN_OK) return st;
   if (fits) {
-    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(kColsThreads), 0, stream, cu,
+    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD)), 0, stream, cu,
                        s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, Pw,
                        state_in, static_cast<TIn*>(o), state_out);
   } else {

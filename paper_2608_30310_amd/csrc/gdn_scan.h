@@ -41,6 +41,12 @@ __device__ __forceinline__ void dma16(const void* src, lds_byte* dst) {
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// Barrier for data exchanged through LDS: waits for this wave's LDS accesses
+// only (not for its outstanding global loads, DMA or stores, as
+// __syncthreads does), and keeps the compiler from moving memory accesses
+// across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Byte offset of byte `byte_in_row` of row `row` in a row tile whose rows hold
 // ROW_BYTES / 16 pieces of 16 bytes, piece p of row R stored at p ^ (R % pieces).
 template <int ROW_BYTES>
@@ -153,10 +159,16 @@ __device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, lds_byt
 // its own MFMAs.  hook(k) runs at the start of region k (the whole-head kernel
 // issues its DMA share there).  With outputs, the chunk's O is left in `pout`:
 // pout[ti][i] = O[16 ti + lane % 16][4 (lane / 16) + i] of the wave's columns.
-template <typename L, int DK, bool FWD, typename Hook>
+// With EXPORT (and FWD false), the wave leaves the outputs to another wave: it
+// writes Delta (four 16-byte tiles per lane) to LDS `xd` before hook(5) and
+// the split of M1 (the next chunk's B operand of K M0, layout [k step][hi |
+// lo][lane]) to `xm` at the end.
+template <typename L, int DK, bool FWD, bool EXPORT, typename Hook>
 __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, const u32x4* pg, int lane,
                                            f32x4 (&M)[DK / 16], Frag (&mb)[DK / 32], f32x4 (&pout)[4],
-                                           Hook&& hook) {
+                                           Hook&& hook, unsigned char* xd = nullptr,
+                                           unsigned char* xm = nullptr) {
+  static_assert(!(FWD && EXPORT), "a wave that exports Delta leaves the outputs to another");
   constexpr bool SPLIT = L::kSplit;
   constexpr int NT = DK / 16, NK = DK / 32;
   constexpr int NKA = ka_frags(DK), NKT = kt_frags(DK);
@@ -300,6 +312,10 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
   //      weighted Delta rows 0..31 (and of Delta for the outputs); K^T
   //      arrives
   ld_kt(kt1, 1);
+  if constexpr (EXPORT) {
+#pragma unroll
+    for (int ti = 0; ti < 2; ++ti) reinterpret_cast<f32x4*>(xd)[ti * kWave + lane] = D[ti];   // final
+  }
 #pragma unroll
   for (int ti = 2; ti < 4; ++ti) D[ti] = mma_x3(tfr[tri_frag(ti, 1)], rb1, D[ti]);
   f32x4 Dw[4];
@@ -315,6 +331,10 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
   if constexpr (FWD) dd0 = chain_frag(D[0], D[1]);
   __builtin_amdgcn_sched_barrier(0);
 
+  if constexpr (EXPORT) {
+#pragma unroll
+    for (int ti = 2; ti < 4; ++ti) reinterpret_cast<f32x4*>(xd)[ti * kWave + lane] = D[ti];
+  }
   hook(5);
   // ---- region 5: M1 partial, k step 0 (tokens 0..31) | split of the
   //      weighted Delta rows 32..63
@@ -357,6 +377,14 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
     M[2 * kk] = mma_a<SPLIT>(kt1[2 * kk], db1, acc[2 * kk]);
     M[2 * kk + 1] = mma_a<SPLIT>(kt1[2 * kk + 1], db1, acc[2 * kk + 1]);
     mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
+  }
+  if constexpr (EXPORT) {
+    u32x4* x = reinterpret_cast<u32x4*>(xm);
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      x[(2 * kk) * kWave + lane] = __builtin_bit_cast(u32x4, mb[kk].hi);
+      x[(2 * kk + 1) * kWave + lane] = __builtin_bit_cast(u32x4, mb[kk].lo);
+    }
   }
 }
 
@@ -424,11 +452,14 @@ __device__ __forceinline__ void store_chunk_out(TIn* o, const ScanUnit& u, int c
 }
 
 // ---------------------------------------------------------------- latency kernel
-// grid = N x Hv x d_v/32: two compute waves (16 columns each) and one wave that
-// only issues DMA, one workgroup per CU.  Used when this grid fits on the chip
-// at once, where per-chunk latency is all that matters.
+// grid = N x Hv x d_v/32, one workgroup per CU.  Used when this grid fits on
+// the chip at once, where per-chunk latency is all that matters.  Tail replay:
+// two compute waves (16 columns each) and one wave that only issues DMA.  With
+// outputs: the two waves that carry the recurrence hand Delta and the split
+// state to two output waves (one per 16 columns), which also issue the DMA,
+// so the outputs' products stay off the sequential chain.
 constexpr int kColsPerGroup = 32;
-constexpr int kColsThreads = 3 * kWave;
+constexpr int cols_threads(bool fwd) { return (fwd ? 4 : 3) * kWave; }
 
 template <typename TIn, int DK, bool FWD>
 using ColsLds = ScanLds<TIn, DK, kColsPerGroup, FWD, true>;
@@ -489,8 +520,8 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
         if (ci > 0) store_chunk_out(o, u, ci - 1, hv, dv, col - lr, lane, pout);
       }
       const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
-      chunk_step<L, DK, FWD>((const unsigned char*)(lds_l + b * L::kBytes), 16 * wave, pg, lane, M, mb, pout,
-                             [](int) {});
+      chunk_step<L, DK, FWD, false>((const unsigned char*)(lds_l + b * L::kBytes), 16 * wave, pg, lane, M, mb,
+                                    pout, [](int) {});
     }
     if (L::kBuffers == 1) {
       __syncthreads();   // the compute waves are done with the only buffer
@@ -515,16 +546,205 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
   }
 }
 
+// LDS of the workgroup with outputs: chunk buffers (P read from global
+// memory) and, per 16-column tile, the exchange from the recurrence wave to
+// the output wave: Delta (4 KiB) and the split state (d_k / 32 x 2 KiB).
+template <typename TIn, int DK>
+struct ColsOutLayout {
+  using L = ScanLds<TIn, DK, kColsPerGroup, true, false>;
+  static constexpr int kDBytes = 4 * kWave * 16;
+  static constexpr int kMBytes = DK / 32 * 2 * kWave * 16;
+  static constexpr int kTileBytes = kDBytes + kMBytes;
+  static constexpr int kBuffers = 2 * L::kBytes + 2 * kTileBytes <= kLdsBytes ? 2 : 1;
+  static constexpr int kOffX = kBuffers * L::kBytes;
+  static constexpr int kBytes = kOffX + 2 * kTileBytes;
+  static_assert(kBytes <= kLdsBytes, "column scan with outputs does not fit in LDS");
+};
+
+// One column-split workgroup with outputs (block `block` of `nblocks`), LDS in
+// `lds_l`.  Waves 0 and 1 carry the recurrence of columns 16 w.. (chunk_step
+// without outputs, exporting Delta before its region 5 and the split of M1 at
+// its end); wave 2 + w writes the outputs of the same columns:
+//   before the mid-chunk barrier: (Q M0)^T from the split M0 of the chunk;
+//   after it: O^T = diag-scaled (Q M0)^T + Delta^T P^T, stored at the start
+//   of the next chunk.
+// Waves 2 and 3 share the next chunk's DMA, half before and half after the
+// mid-chunk barrier.  The products are those of chunk_step with outputs, in
+// the same order, so the results are the same bit for bit.
+template <typename TIn, int DK>
+__device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, int nblocks,
+                                                   const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
+                                                   int32_t dv, const TIn* __restrict__ v,
+                                                   const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                                                   const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
+                                                   const float* __restrict__ state_in, TIn* __restrict__ o,
+                                                   float* __restrict__ state_out) {
+  using CL = ColsOutLayout<TIn, DK>;
+  using L = typename CL::L;
+  constexpr bool SPLIT = L::kSplit;
+  constexpr int NT = DK / 16, NK = DK / 32;
+  constexpr int NKA = ka_frags(DK), NKT = kt_frags(DK);
+  constexpr int NKF = L::kKFrags;
+  static_assert(L::kKJobs % 2 == 0 && L::kTJobs % 2 == 0 && L::kPJobs == 0 && L::kVJobs % 2 == 0,
+                "DMA halves need records of whole multiples of 2 KiB");
+  constexpr int kHalf = (L::kKJobs + L::kTJobs + L::kVJobs) / 2;   // jobs per output wave, scalars aside
+  const int tid = threadIdx.x;
+  // wave index made provably uniform: DMA destinations (M0) stay scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const bool out_wave = wave >= 2;
+  const int tile = wave & 1, h = wave & 1;
+  const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
+  const int ngroups = dv / kColsPerGroup;
+  // logical unit: the column groups of a value head, then the value heads of a
+  // key head, are adjacent (same XCD, shared records in its L2)
+  const int unit = xcd_remap(block, nblocks);
+  const int col0 = kColsPerGroup * (unit % ngroups);
+  const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
+  const int colw = col0 + 16 * tile;
+  const int64_t vrow = static_cast<int64_t>(hv) * dv;
+  unsigned char* xd = (unsigned char*)(lds_l + CL::kOffX + tile * CL::kTileBytes);
+  unsigned char* xm = xd + CL::kDBytes;
+
+  // jobs 2 q + h of the K record, the T record and the V rows for q in
+  // [q0, q1) (every record is a multiple of two jobs, so which record a job
+  // reads is known at compile time); the scalars with the second half
+  auto dma_half = [&](int ci, int b, int q0, int q1) __attribute__((always_inline)) {
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
+    lds_byte* dst = lds_l + b * L::kBytes;
+#pragma unroll
+    for (int q = q0; q < q1; ++q) {
+      if (q < L::kKJobs / 2) {
+        const int j = 2 * q + h;
+        dma16(c.krec + 1024 * j + 16 * lane, dst + L::kOffK + 1024 * j);
+      } else if (q < (L::kKJobs + L::kTJobs) / 2) {
+        const int j = 2 * (q - L::kKJobs / 2) + h;
+        dma16(c.trec + 1024 * j + 16 * lane, dst + L::kOffT + 1024 * j);
+      } else {
+        // V rows; pad rows repeat the last row (their beta is 0, so they add nothing)
+        dma_rows<L::kVRowBytes>(static_cast<const TIn*>(c.v0), vrow, c.clen, dst + L::kOffV,
+                                2 * (q - (L::kKJobs + L::kTJobs) / 2) + h, lane);
+      }
+    }
+    if (q1 == kHalf) {
+      if (h == 0) dma16(c.srow + 16 * lane, dst + L::kOffS);                          // bytes 0..1023
+      else if (lane < 16) dma16(c.srow + 1024 + 16 * lane, dst + L::kOffS + 1024);    // 1024..1279
+    }
+  };
+
+  f32x4 M[NT];
+  Frag mb[NK];
+  f32x4 pout[4];
+  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * dv + colw + lr;
+  if (!out_wave) {
+    load_state<DK>(state_in, sbase, dv, lg, M, mb);
+    u32x4* x = reinterpret_cast<u32x4*>(xm);
+#pragma unroll
+    for (int kk = 0; kk < NK; ++kk) {
+      x[(2 * kk) * kWave + lane] = __builtin_bit_cast(u32x4, mb[kk].hi);
+      x[(2 * kk + 1) * kWave + lane] = __builtin_bit_cast(u32x4, mb[kk].lo);
+    }
+  } else if (u.nch > 0) {
+    dma_half(0, 0, 0, kHalf);
+    wait_dma();
+  }
+  __syncthreads();
+  for (int ci = 0; ci < u.nch; ++ci) {
+    const int b = CL::kBuffers == 2 ? (ci & 1) : 0;
+    const unsigned char* base = (const unsigned char*)(lds_l + b * L::kBytes);
+    const bool prefetch = CL::kBuffers == 2 && ci + 1 < u.nch;
+    if (!out_wave) {
+      chunk_step<L, DK, false, true>(base, 16 * tile, nullptr, lane, M, mb, pout,
+                                     [](int k) __attribute__((always_inline)) {
+                                       if (k == 5) lds_barrier();   // Delta is out
+                                     },
+                                     xd, xm);
+    } else {
+      if (ci > 0) store_chunk_out(o, u, ci - 1, hv, dv, colw, lane, pout);
+      if (prefetch) dma_half(ci + 1, b ^ 1, 0, kHalf / 2);
+      // (Q M0)^T: A = split M0 from the recurrence wave, B = Q fragments
+      const u32x4* kf = reinterpret_cast<const u32x4*>(base + L::kOffK);
+      const u32x4* x = reinterpret_cast<const u32x4*>(xm);
+      Frag m0[NK], qa[4][NK];
+#pragma unroll
+      for (int kk = 0; kk < NK; ++kk) {
+        m0[kk].hi = __builtin_bit_cast(bf16x8, x[(2 * kk) * kWave + lane]);
+        m0[kk].lo = __builtin_bit_cast(bf16x8, x[(2 * kk + 1) * kWave + lane]);
+      }
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+          const int f = NKA + NKT + ti * NK + kk;
+          qa[ti][kk].hi = __builtin_bit_cast(bf16x8, kf[f * kWave + lane]);
+          if constexpr (SPLIT) qa[ti][kk].lo = __builtin_bit_cast(bf16x8, kf[(NKF + f) * kWave + lane]);
+        }
+      f32x4 qm[4];
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti) {
+        qm[ti] = zero4();
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) qm[ti] = mma_b<SPLIT>(m0[kk], qa[ti][kk], qm[ti]);
+      }
+      // P (split, six nonzero fragments) from global memory
+      const u32x4* pg = Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave);
+      Frag pfr[kTFrags];
+#pragma unroll
+      for (int f = 0; f < kTFrags; ++f) {
+        pfr[f].hi = __builtin_bit_cast(bf16x8, pg[f * kWave + lane]);
+        pfr[f].lo = __builtin_bit_cast(bf16x8, pg[(kTFrags + f) * kWave + lane]);
+      }
+      lds_barrier();   // Delta is in
+      const f32x4* xdv = reinterpret_cast<const f32x4*>(xd);
+      f32x4 D[4];
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti) D[ti] = xdv[ti * kWave + lane];
+      const Frag dd0 = chain_frag(D[0], D[1]);
+      const Frag dd1 = chain_frag(D[2], D[3]);
+      const float* sc = reinterpret_cast<const float*>(base + L::kOffS);
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti) {
+        const float qe = sc[3 * kChunk + 16 * ti + lr];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) pout[ti][r] = qe * qm[ti][r];
+        pout[ti] = mma_x3(dd0, pfr[tri_frag(ti, 0)], pout[ti]);
+        if (ti >= 2) pout[ti] = mma_x3(dd1, pfr[tri_frag(ti, 1)], pout[ti]);
+      }
+      if (prefetch) dma_half(ci + 1, b ^ 1, kHalf / 2, kHalf);
+    }
+    if (CL::kBuffers == 1) {
+      __syncthreads();   // every wave is done with the only buffer
+      if (out_wave && ci + 1 < u.nch) dma_half(ci + 1, 0, 0, kHalf);
+    }
+    if (out_wave) wait_dma();
+    __syncthreads();     // next chunk's operands are in LDS; this buffer is free
+  }
+  if (out_wave) {
+    if (u.nch > 0) store_chunk_out(o, u, u.nch - 1, hv, dv, colw, lane, pout);
+  } else if (state_out) {
+#pragma unroll
+    for (int td = 0; td < NT; ++td)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] = M[td][r];
+  }
+}
+
 template <typename TIn, int DK, bool FWD>
-__global__ __launch_bounds__(kColsThreads) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(cols_threads(FWD)) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
                  const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                  const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                  const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
-  using L = ColsLds<TIn, DK, FWD>;
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
-  scan_cols_body<TIn, DK, FWD>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw, Sw, Pw,
-                               state_in, o, state_out);
+  if constexpr (FWD) {
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[ColsOutLayout<TIn, DK>::kBytes];
+    scan_cols_out_body<TIn, DK>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw, Sw, Pw,
+                                state_in, o, state_out);
+  } else {
+    using L = ColsLds<TIn, DK, false>;
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+    scan_cols_body<TIn, DK, false>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw, Sw, Pw,
+                                   state_in, o, state_out);
+  }
 }
 
 // ---------------------------------------------------------------- replay scan + suffix intra
@@ -621,7 +841,8 @@ void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
       }
     };
     const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
-    chunk_step<L, DK, FWD>((const unsigned char*)(lds + b * L::kBytes), 16 * wave, pg, lane, M, mb, pout, hook);
+    chunk_step<L, DK, FWD, false>((const unsigned char*)(lds + b * L::kBytes), 16 * wave, pg, lane, M, mb, pout,
+                                  hook);
     if (L::kBuffers == 1) {
       __syncthreads();   // every wave is done with the only buffer
       if (ci + 1 < u.nch) dma_share(ci + 1, 0, 0, PER_WAVE);
