@@ -580,6 +580,95 @@ def sweep(args):
           "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
           "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
 
+    # ---- decode steps after the rebuild: one token per sequence from the state,
+    #      state updated in place; HBM-bound (the state is read and written once,
+    #      with streaming loads and stores).  Timed as a HIP graph of 20 launches
+    #      (no host overhead per step); the 1-sequence line is the first token's
+    #      latency after a hit, the others are batched decode throughput.
+    for nb in (1, 64, 256):
+        xd = random_dev([1] * nb, 16, 32, 128, seed=900 + nb)
+        sd = torch.randn((nb, 32, 128, 128), dtype=torch.float32, device=dev) * 0.1
+        od = torch.empty((nb, 32, 128), dtype=torch.bfloat16, device=dev)
+        calls = 20
+        dec = lambda: [gdn.decode_step(xd["q"], xd["k"], xd["v"], xd["g"], xd["beta"], state_in=sd,
+                                       state_out=sd, o=od, scale=128 ** -0.5) for _ in range(calls)]
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            dec()
+        torch.cuda.current_stream().wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            dec()
+        t = timed_us(graph.replay)
+        per = t["p50"] / calls
+        nbytes = (2 * nb * 32 * 128 * 128 * 4 + 2 * nb * 16 * 128 * 2 + 2 * nb * 32 * 128 * 2
+                  + 2 * nb * 32 * 4)
+        emit({"workload": f"decode step Hk=16 Hv=32 d=128 bf16, {nb} sequences, state in place",
+              "us_per_step": per, "tokens_per_s": nb / (per * 1e-6),
+              "gbs": nbytes / (per * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (per * 1e-6) / 1e9 / HBM_PEAK_GBS,
+              "note": f"graph of {calls} launches per timed rep"})
+
+    # ---- FA-KV transfer overlapped with the replay (paper Section 3, "Replay
+    #      efficiency"): a hit of m tokens moves the full-attention KV of the
+    #      matched prefix from pinned host memory while the linear-attention
+    #      layers replay their tails; the transfer joins the compute stream only
+    #      before the suffix forward.  Synthetic sizes: 24 GDN layers
+    #      (Hk=16, Hv=32, d=128) and 32 KiB of FA KV per token (8 FA layers x
+    #      K, V x 4 KV heads x 256 x bf16).  H2D-SER: copy, replays, forwards on
+    #      one stream; H2D-OVL: copy on a second stream beside the replays.
+    n_la, kv_per_token = 24, 32 << 10
+    copy_stream = torch.cuda.Stream()
+    for m in (8192, 32768):
+        r = {8192: 819, 32768: 3277}[m]
+        host_kv = torch.empty(m * kv_per_token, dtype=torch.uint8, pin_memory=True)
+        dev_kv = torch.empty(m * kv_per_token, dtype=torch.uint8, device=dev)
+        xl = [random_dev([r], 16, 32, 128, seed=2000 + l) for l in range(n_la)]
+        xq = [random_dev([512], 16, 32, 128, seed=3000 + l) for l in range(n_la)]
+        wst, st, _ = buffers(xl[0], 1, 16, 32, 128, False)
+        wsf, st2, o = buffers(xq[0], 1, 16, 32, 128, True)
+
+        def replays():
+            for x in xl:
+                replay(x, st, wst)
+
+        def forwards():
+            for x in xq:
+                forward(x, st, o, st2, wsf)
+
+        def h2d(stream):
+            with torch.cuda.stream(stream):
+                dev_kv.copy_(host_kv, non_blocking=True)
+
+        main = torch.cuda.current_stream()
+
+        def serial():
+            h2d(main)
+            replays()
+            forwards()
+
+        def overlapped():
+            copy_stream.wait_stream(main)
+            h2d(copy_stream)
+            replays()
+            main.wait_stream(copy_stream)
+            forwards()
+
+        t_h2d = timed_us(lambda: h2d(main))
+        t_rep = timed_us(replays)
+        t_fwd = timed_us(forwards)
+        t_ser = timed_us(serial)
+        t_ovl = timed_us(overlapped)
+        hidden = (t_ser["p50"] - t_ovl["p50"]) / min(t_h2d["p50"], t_rep["p50"])
+        emit({"workload": f"FA-KV H2D overlapped with replay, m={m}, r={r}, {n_la} GDN layers, "
+                          f"{m * kv_per_token >> 20} MiB FA KV, suffix 512",
+              "h2d_us": t_h2d["p50"], "h2d_gbs": m * kv_per_token / (t_h2d["p50"] * 1e-6) / 1e9,
+              "replay_us": t_rep["p50"], "suffix_forward_us": t_fwd["p50"],
+              "h2d_ser_us": t_ser["p50"], "h2d_ovl_us": t_ovl["p50"],
+              "ovl_vs_ser_reduction": 1 - t_ovl["p50"] / t_ser["p50"],
+              "hidden_fraction_of_shorter": hidden})
+        del host_kv, dev_kv, xl, xq
+
     # ---- replay vs full prefill, suffix 512: t_full = forward(0, m + s) with
     #      outputs; t_replay = the fused replay(r) + forward(S_m, s); state-only
     #      full = replay(m + s)

@@ -203,6 +203,24 @@ int32_t gdn_replay_forward_num_stages(void);
 const char* gdn_replay_forward_stage_name(int32_t stage);
 
 /*
+ * One decode step (paper Section 2, Eq. 1 applied to a single new token; the
+ * tokens generated after the prefix state has been rebuilt, Section 3).  For
+ * each sequence n (num_seqs = N, one token each) and value head h, with
+ * alpha = exp(g):
+ *     M1 = alpha M + k (beta (v - alpha M^T k))^T,   o = scale M1^T q.
+ *   q, k [N,Hk,d_k], v [N,Hv,d_v] (qkv_dtype); g, beta [N,Hv] fp32;
+ *   state_in [N,Hv,d_k,d_v] fp32 (NULL = zero state); state_out (required;
+ *   may equal state_in, must not otherwise overlap it); o [N,Hv,d_v].
+ * No workspace; one kernel on `stream`.  q, k, v, o and the states must be
+ * 16-byte aligned (GDN_ERR_UNSUPPORTED otherwise); N = 0 does nothing.
+ */
+gdn_status gdn_decode_step(const gdn_shape* shape,
+                           const void* q, const void* k, const void* v,
+                           const float* g, const float* beta,
+                           const float* state_in, void* o, float* state_out,
+                           void* stream);
+
+/*
  * Replay budget of the paper (Section 3): k = ceil(r * m) for a ratio
  * r = ratio_num / ratio_den, in exact integer arithmetic.  Returns -1 when
  * m < 0, ratio_num < 0, ratio_den <= 0 or the product overflows.

@@ -76,6 +76,8 @@ def load_library():
     lib.gdn_num_stages.restype = ctypes.c_int32
     lib.gdn_stage_name.argtypes = [ctypes.c_int32, ctypes.c_int32]
     lib.gdn_stage_name.restype = ctypes.c_char_p
+    lib.gdn_decode_step.argtypes = [SP, P, P, P, P, P, P, P, P, P]
+    lib.gdn_decode_step.restype = ctypes.c_int
     lib.gdn_replay_len.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
     lib.gdn_replay_len.restype = ctypes.c_int64
     lib.gdn_status_string.argtypes = [ctypes.c_int]
@@ -397,3 +399,51 @@ def replay_forward(k_tail: torch.Tensor, v_tail: torch.Tensor, g_tail: torch.Ten
         arr, ne = _event_array(events, True, fused=True)
         _check(lib.gdn_replay_forward_profiled(*args, ctypes.cast(arr, ctypes.c_void_p), ne))
     return o, state_mid, state_out
+
+
+def decode_step(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tensor,
+                beta: torch.Tensor, state_in: Optional[torch.Tensor] = None, scale: float = 1.0,
+                o: Optional[torch.Tensor] = None, state_out: Optional[torch.Tensor] = None):
+    """One decode step (paper Section 2, Eq. 1 for a single token per sequence)
+    on torch's current stream.
+
+    q, k [N,Hk,d_k], v [N,Hv,d_v] (bf16 or fp32), g/beta [N,Hv] fp32,
+    state_in [N,Hv,d_k,d_v] fp32 (None = zero state).  Returns
+    ``(o [N,Hv,d_v], state_out)``; pass ``state_out=state_in`` to update in place.
+    """
+    lib = load_library()
+    device = q.device
+    dt = q.dtype
+    _need(q, "q", dt, device, 3)
+    _need(k, "k", dt, device, 3)
+    _need(v, "v", dt, device, 3)
+    n, hk, dk = q.shape
+    if tuple(k.shape) != (n, hk, dk):
+        raise ValueError("q and k must have the same shape")
+    hv, dv = v.shape[1], v.shape[2]
+    if v.shape[0] != n:
+        raise ValueError("v must hold one token per sequence, like q and k")
+    _need(g, "g", torch.float32, device, 2)
+    _need(beta, "beta", torch.float32, device, 2)
+    if tuple(g.shape) != (n, hv) or tuple(beta.shape) != (n, hv):
+        raise ValueError("g and beta must be [N, Hv]")
+    if state_in is not None:
+        _need(state_in, "state_in", torch.float32, device, 4)
+        if tuple(state_in.shape) != (n, hv, dk, dv):
+            raise ValueError("state_in must be [N, Hv, d_k, d_v]")
+    if state_out is None:
+        state_out = torch.empty((n, hv, dk, dv), dtype=torch.float32, device=device)
+    _need(state_out, "state_out", torch.float32, device, 4)
+    if tuple(state_out.shape) != (n, hv, dk, dv):
+        raise ValueError("state_out must be [N, Hv, d_k, d_v]")
+    if o is None:
+        o = torch.empty((n, hv, dv), dtype=dt, device=device)
+    _need(o, "o", dt, device, 3)
+    if tuple(o.shape) != (n, hv, dv):
+        raise ValueError("o must be [N, Hv, d_v]")
+    shp = _shape(n, hk, hv, dk, dv, _dtype_code(q), scale)
+    stream = torch.cuda.current_stream(device)
+    _check(lib.gdn_decode_step(ctypes.byref(shp), _ptr(q), _ptr(k), _ptr(v), _ptr(g), _ptr(beta),
+                               _ptr(state_in), _ptr(o), _ptr(state_out),
+                               ctypes.c_void_p(stream.cuda_stream)))
+    return o, state_out

@@ -22,6 +22,7 @@
 #include <limits>
 #include <string>
 
+#include "gdn_decode.h"
 #include "gdn_intra.h"
 #include "gdn_plan.h"
 #include "gdn_scan.h"
@@ -398,6 +399,57 @@ gdn_status replay_forward_impl(const gdn_shape* shape, const int32_t* cu_tail_ho
 }  // namespace
 }  // namespace gdn
 
+namespace gdn {
+namespace {
+
+template <typename TIn, int DK, int DV>
+void launch_decode(const gdn_shape& s, const void* q, const void* k, const void* v, const float* g,
+                   const float* beta, const float* state_in, void* o, float* state_out, hipStream_t stream) {
+  const uint32_t blocks = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads;
+  hipLaunchKernelGGL((k_decode<TIn, DK, DV>), dim3(blocks), dim3(kDecodeThreads), 0, stream, s.num_k_heads,
+                     s.num_v_heads, static_cast<const TIn*>(q), static_cast<const TIn*>(k),
+                     static_cast<const TIn*>(v), g, beta, s.scale, state_in, static_cast<TIn*>(o), state_out);
+}
+
+template <typename TIn>
+void decode_dims(const gdn_shape& s, const void* q, const void* k, const void* v, const float* g,
+                 const float* beta, const float* state_in, void* o, float* state_out, hipStream_t stream) {
+  if (s.d_k == 64) {
+    if (s.d_v == 64) launch_decode<TIn, 64, 64>(s, q, k, v, g, beta, state_in, o, state_out, stream);
+    else launch_decode<TIn, 64, 128>(s, q, k, v, g, beta, state_in, o, state_out, stream);
+  } else {
+    if (s.d_v == 64) launch_decode<TIn, 128, 64>(s, q, k, v, g, beta, state_in, o, state_out, stream);
+    else launch_decode<TIn, 128, 128>(s, q, k, v, g, beta, state_in, o, state_out, stream);
+  }
+}
+
+gdn_status decode_step_impl(const gdn_shape* shape, const void* q, const void* k, const void* v,
+                            const float* g, const float* beta, const float* state_in, void* o,
+                            float* state_out, void* stream) {
+  std::string err;
+  const gdn_status st = check_shape(shape, &err);
+  if (st != GDN_OK) return fail(st, err);
+  if (shape->num_seqs == 0) return GDN_OK;
+  if (!q || !k || !v || !g || !beta || !o || !state_out)
+    return fail(GDN_ERR_NULL_ARG, "q, k, v, g, beta, o and state_out must be non-NULL");
+  auto misaligned = [](const void* p) { return reinterpret_cast<uintptr_t>(p) % 16 != 0; };
+  if (misaligned(q) || misaligned(k) || misaligned(v) || misaligned(o) || misaligned(state_out) ||
+      (state_in && misaligned(state_in)))
+    return fail(GDN_ERR_UNSUPPORTED, "q, k, v, o and the states must be 16-byte aligned");
+  if (state_in && state_in != state_out) {
+    const size_t n = static_cast<size_t>(shape->num_seqs) * shape->num_v_heads * shape->d_k * shape->d_v;
+    if (state_in < state_out + n && state_out < state_in + n)
+      return fail(GDN_ERR_BAD_SHAPE, "state_out overlaps state_in without being equal");
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (shape->qkv_dtype == GDN_BF16) decode_dims<uint16_t>(*shape, q, k, v, g, beta, state_in, o, state_out, s);
+  else decode_dims<float>(*shape, q, k, v, g, beta, state_in, o, state_out, s);
+  return check_launch("decode launch");
+}
+
+}  // namespace
+}  // namespace gdn
+
 extern "C" {
 
 gdn_status gdn_tail_replay(const gdn_shape* shape, const int32_t* cu_seqlens_host,
@@ -476,6 +528,12 @@ gdn_status gdn_replay_forward_profiled(const gdn_shape* shape, const int32_t* cu
   return gdn::replay_forward_impl(shape, cu_tail_host, cu_tail, k_tail, v_tail, g_tail, beta_tail, cu_suf_host,
                                   cu_suf, q, k, v, g, beta, state_mid, o, state_out, workspace, workspace_bytes,
                                   stream, stage_events);
+}
+
+gdn_status gdn_decode_step(const gdn_shape* shape, const void* q, const void* k, const void* v,
+                           const float* g, const float* beta, const float* state_in, void* o,
+                           float* state_out, void* stream) {
+  return gdn::decode_step_impl(shape, q, k, v, g, beta, state_in, o, state_out, stream);
 }
 
 int32_t gdn_replay_forward_num_stages(void) { return gdn::kNumFusedStages; }

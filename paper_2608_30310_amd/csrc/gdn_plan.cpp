@@ -12,12 +12,12 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 bool supported_dim(int32_t d) { return d == 64 || d == 128; }
 
+constexpr int64_t kMaxGroups = std::numeric_limits<uint32_t>::max() / 256;
+
 }  // namespace
 
-gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_outputs,
-                     Plan* plan, std::string* err) {
+gdn_status check_shape(const gdn_shape* shape, std::string* err) {
   if (!shape) { *err = "shape is NULL"; return GDN_ERR_NULL_ARG; }
-  if (!plan) { *err = "plan is NULL"; return GDN_ERR_NULL_ARG; }
   const int32_t N = shape->num_seqs, hk = shape->num_k_heads, hv = shape->num_v_heads;
   if (N < 0) { *err = "num_seqs must be >= 0"; return GDN_ERR_BAD_SHAPE; }
   if (hk < 1 || hv < 1) { *err = "head counts must be >= 1"; return GDN_ERR_BAD_SHAPE; }
@@ -36,6 +36,21 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   }
   if (!std::isfinite(shape->scale)) { *err = "scale must be finite"; return GDN_ERR_BAD_SHAPE; }
   if (hv > 65535) { *err = "num_v_heads must be <= 65535"; return GDN_ERR_UNSUPPORTED; }
+  // A grid dimension counts at most 2^32 - 1 work items; every kernel uses at
+  // most 256 threads per workgroup and at most 4 workgroups per (sequence, head).
+  if (static_cast<int64_t>(N) * hv * 4 > kMaxGroups) {
+    *err = "num_seqs * num_v_heads too large";
+    return GDN_ERR_UNSUPPORTED;
+  }
+  return GDN_OK;
+}
+
+gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_outputs,
+                     Plan* plan, std::string* err) {
+  if (!plan) { *err = "plan is NULL"; return GDN_ERR_NULL_ARG; }
+  const gdn_status st = check_shape(shape, err);
+  if (st != GDN_OK) return st;
+  const int32_t N = shape->num_seqs, hk = shape->num_k_heads, hv = shape->num_v_heads;
   if (!cu) { *err = "cu_seqlens_host is NULL"; return GDN_ERR_NULL_ARG; }
   if (cu[0] != 0) { *err = "cu_seqlens_host[0] must be 0"; return GDN_ERR_BAD_SEQLENS; }
 
@@ -55,14 +70,6 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
     *err = "too many chunks";
     return GDN_ERR_UNSUPPORTED;
   }
-  // A grid dimension counts at most 2^32 - 1 work items; every kernel uses at
-  // most 256 threads per workgroup and at most 4 workgroups per (sequence, head).
-  constexpr int64_t kMaxGroups = std::numeric_limits<uint32_t>::max() / 256;
-  if (static_cast<int64_t>(N) * hv * 4 > kMaxGroups) {
-    *err = "num_seqs * num_v_heads too large";
-    return GDN_ERR_UNSUPPORTED;
-  }
-
   if (slots > kMaxGroups) {
     *err = "too many chunk slots";
     return GDN_ERR_UNSUPPORTED;

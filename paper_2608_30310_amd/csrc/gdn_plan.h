@@ -56,6 +56,9 @@ struct Plan {
   size_t bytes = 0;               // total workspace size
 };
 
+// Validates the shape alone (dimensions, dtype, scale, grid limits).
+gdn_status check_shape(const gdn_shape* shape, std::string* err);
+
 // Validates the shape and the host copy of the offsets and fills `plan`.
 // Returns GDN_OK or a validation status with a message in `err`.
 gdn_status make_plan(const gdn_shape* shape, const int32_t* cu_seqlens_host,

@@ -11,7 +11,8 @@ are run against the oracle (all must hold) and against planted mistakes (each
 must break at least one), so together they cover every term of Eq. 1.
 
 Sources of each fact:
-  * closed forms of Eq. 1 (paper Section 2) for one and two tokens, a worked
+  * closed forms of Eq. 1 (paper Section 2) for one and two tokens and for
+    one token from a nonzero state (a decode step), a worked
     two-token example with hand-derived decimals, the textbook delta rule
     (alpha = beta = 1), pure decay (beta = 0) and the identity step;
   * Eq. 2 (Section 3): replaying the whole prefix from zero is full prefill;
@@ -122,6 +123,28 @@ def pin_two_tokens(fn):
     want = (a2 * beta[0] * np.outer(v[0], k[0]) @ (np.eye(dk) - beta[1] * np.outer(k[1], k[1]))
             + beta[1] * np.outer(v[1], k[1]))
     _close(S, want, what="two-token state")
+
+
+def pin_decode_step(fn):
+    """One token from a nonzero state (a decode step): S1 = alpha S0 (I - beta k k^T)
+    + beta v k^T and o = scale S1 q, for several batched (sequence, head) pairs."""
+    rng = _rng(19)
+    dk, dv, n, hk, hv = 5, 3, 3, 1, 2
+    k = _unit(rng, n, hk, dk)
+    q = rng.standard_normal((n, hk, dk))
+    v = rng.standard_normal((n, hv, dv))
+    g = rng.uniform(-1.0, 0.0, (n, hv))
+    beta = rng.uniform(0.05, 1.0, (n, hv))
+    M0 = rng.standard_normal((n, hv, dk, dv))          # state = S^T
+    o, M = fn(k, v, g, beta, np.arange(n + 1), q=q, state_in=M0, scale=0.7)
+    for s in range(n):
+        for h in range(hv):
+            kk, qq = k[s, 0], q[s, 0]
+            S0 = M0[s, h].T
+            S1 = (np.exp(g[s, h]) * S0 @ (np.eye(dk) - beta[s, h] * np.outer(kk, kk))
+                  + beta[s, h] * np.outer(v[s, h], kk))
+            _close(M[s, h].T, S1, what="decode-step state")
+            _close(o[s, h], 0.7 * S1 @ qq, what="decode-step output")
 
 
 def pin_identity_step(fn):
@@ -319,7 +342,7 @@ def pin_tail_error(fn):
 
 
 ALL_PINS = [
-    pin_single_token, pin_worked_example, pin_two_tokens, pin_identity_step,
+    pin_single_token, pin_worked_example, pin_two_tokens, pin_decode_step, pin_identity_step,
     pin_delta_rule_textbook, pin_pure_decay, pin_product_formula,
     pin_chunked_form, pin_linearity, pin_grouped_heads, pin_varlen,
     pin_continuation, pin_norm_bound, pin_tail_replay_full, pin_tail_error,

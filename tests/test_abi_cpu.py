@@ -153,6 +153,31 @@ def test_chunk_forward_rejects_before_launch(case):
     assert st == want, lib.gdn_last_error().decode()
 
 
+@needs_no_gpu
+@pytest.mark.parametrize("case", ["null_q", "null_o", "null_state_out", "overlap", "misaligned_state",
+                                  "misaligned_v", "bad_dk", "bad_dtype", "bad_heads"])
+def test_decode_step_rejects_before_launch(case):
+    lib = gdn.load_library()
+    kw = {"bad_dk": dict(d_k=96), "bad_dtype": dict(qkv_dtype=7), "bad_heads": dict(num_k_heads=3)}
+    shape = _shape(num_seqs=2, **kw.get(case, {}))
+    state_bytes = 2 * 32 * 128 * 128 * 4
+    s_in = ctypes.c_void_p(0x100000 + (4 if case == "misaligned_state" else 0))
+    s_out = ctypes.c_void_p(0x100000 + (state_bytes // 2 if case == "overlap" else 2 * state_bytes))
+    st = lib.gdn_decode_step(ctypes.byref(shape), None if case == "null_q" else FAKE, FAKE,
+                             ctypes.c_void_p(0x1008) if case == "misaligned_v" else FAKE, FAKE, FAKE,
+                             s_in, None if case == "null_o" else FAKE,
+                             None if case == "null_state_out" else s_out, None)
+    want = {"null_q": 1, "null_o": 1, "null_state_out": 1, "overlap": 2, "misaligned_state": 4,
+            "misaligned_v": 4, "bad_dk": 4, "bad_dtype": 4, "bad_heads": 2}[case]
+    assert st == want, lib.gdn_last_error().decode()
+
+
+def test_decode_step_with_no_sequences_does_nothing():
+    lib = gdn.load_library()
+    assert lib.gdn_decode_step(ctypes.byref(_shape(num_seqs=0)), None, None, None, None, None,
+                               None, None, None, None) == 0
+
+
 def test_status_strings():
     lib = gdn.load_library()
     for code in range(7):
