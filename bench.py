@@ -43,12 +43,13 @@ METRIC = "GDN tail-replay tokens/sec/GPU + state-rebuild latency; % of MFMA roof
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 CHUNK = 64
-CALIB_BYTES = 256 << 20        # plain copy used to calibrate the PMC byte counters
+CALIB_BYTES = 1 << 30          # plain copy used to calibrate the PMC byte counters (> the 256 MB MALL)
 FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload1_r{r}.json")
 KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
                   "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
                   "paper_2608_30310_amd/csrc/gdn_intra.h", "paper_2608_30310_amd/csrc/gdn_scan.h",
+                  "paper_2608_30310_amd/csrc/gdn_decode.h",
                   "paper_2608_30310_amd/csrc/gdn_api.hip", "paper_2608_30310_amd/build.py")
 
 
@@ -68,9 +69,19 @@ def parse():
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run plain device copies of a known size (PMC calibration)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
+    ap.add_argument("--pmc-out", default=None,
+                    help="with --summarize-pmc: output .json (default: the default workload's file)")
+    ap.add_argument("--pmc-workload", default=None,
+                    help="with --summarize-pmc: workload description stored in the summary")
     ap.add_argument("--sweep", action="store_true",
                     help="time the other workloads instead (one JSON line each): small fp32 layer, "
-                         "36-layer stack, 16 varlen hits, replay-vs-full at 8K/16K/32K")
+                         "36-layer stack, 16 varlen hits, decode steps, FA-KV transfer overlap, "
+                         "replay-vs-full at 8K/16K/32K")
+    ap.add_argument("--only", default="",
+                    help="with --sweep: comma list of sections to run "
+                         "(small, layer410, stack, hits, decode, h2d, full)")
+    ap.add_argument("--decode-seqs", default="1,64,256",
+                    help="with --sweep: batch sizes of the decode lines")
     return ap.parse_args()
 
 
@@ -116,43 +127,61 @@ def _counter_rows(d):
     return rows
 
 
-def _per_kernel_mean(rows, counter):
-    """Mean over dispatches of the counter, per kernel name (KiB per dispatch)."""
+def _per_dispatch(rows, counter):
+    """{(kernel name, grid size): [counter value per dispatch, KiB]}."""
     per = {}
     for r in rows:
         if r.get("Counter_Name") != counter:
             continue
-        key = (r["Kernel_Name"], r.get("Dispatch_Id") or r.get("Correlation_Id"))
+        key = (r["Kernel_Name"], int(r.get("Grid_Size") or 0), r.get("Dispatch_Id") or r.get("Correlation_Id"))
         per[key] = per.get(key, 0.0) + float(r["Counter_Value"])
     out = {}
-    for (name, _), v in per.items():
-        out.setdefault(name, []).append(v)
+    for (name, grid, _), v in per.items():
+        out.setdefault((name, grid), []).append(v)
+    return out
+
+
+def _per_kernel_mean(rows, counter):
+    """Mean over dispatches of the counter, per kernel name (KiB per dispatch)."""
+    out = {}
+    for (name, _), v in _per_dispatch(rows, counter).items():
+        out.setdefault(name, []).extend(v)
     return {name: statistics.fmean(v) for name, v in out.items()}
 
 
-def summarize_pmc(fetch_dir, write_dir, replay):
-    fetch = _per_kernel_mean(_counter_rows(fetch_dir), "FETCH_SIZE")
-    write = _per_kernel_mean(_counter_rows(write_dir), "WRITE_SIZE")
-    copy = [n for n in fetch if "neg" in n and "gdn" not in n]
-    if not copy:
-        raise SystemExit("no calibration kernel in the FETCH_SIZE run: rerun bench.py with --calib-copy")
+def _calibration(rows, counter):
+    """The calibration copy's mean reading: dispatches of the elementwise `neg`
+    kernel with the largest grid (other, smaller `neg` launches of the same
+    process do not count)."""
+    cands = {k: v for k, v in _per_dispatch(rows, counter).items() if "neg" in k[0] and "gdn" not in k[0]}
+    if not cands:
+        raise SystemExit(f"no calibration kernel in the {counter} run: rerun bench.py with --calib-copy")
+    key = max(cands, key=lambda k: k[1])
+    return key[0], statistics.fmean(cands[key])
+
+
+def summarize_pmc(fetch_dir, write_dir, replay, out_path=None, workload=None):
+    frows, wrows = _counter_rows(fetch_dir), _counter_rows(write_dir)
+    fetch = _per_kernel_mean(frows, "FETCH_SIZE")
+    write = _per_kernel_mean(wrows, "WRITE_SIZE")
     # the calibration kernel reads and writes CALIB_BYTES
-    cname = max(copy, key=lambda n: fetch[n])
-    f_fetch = CALIB_BYTES / (fetch[cname] * 1024.0)
-    f_write = CALIB_BYTES / (write[cname] * 1024.0)
+    cname, cal_fetch = _calibration(frows, "FETCH_SIZE")
+    _, cal_write = _calibration(wrows, "WRITE_SIZE")
+    f_fetch = CALIB_BYTES / (cal_fetch * 1024.0)
+    f_write = CALIB_BYTES / (cal_write * 1024.0)
     kernels = {}
     for name in fetch:
-        if "k_scan" not in name and "k_intra" not in name:
+        if not any(t in name for t in ("k_scan", "k_intra", "k_decode")):
             continue
         short = name.split("(")[0].replace("void ", "")
         fb = fetch[name] * 1024.0 * f_fetch
         wb = write.get(name, 0.0) * 1024.0 * f_write
         kernels[short] = {"fetch_kib": fetch[name], "write_kib": write.get(name, 0.0),
                           "fetch_bytes": fb, "write_bytes": wb, "traffic_bytes": fb + wb}
-    summary = {"workload": f"one layer Hk=16 Hv=32 d=128 bf16, tail {replay} + suffix 512",
+    summary = {"workload": workload or f"one layer Hk=16 Hv=32 d=128 bf16, tail {replay} + suffix 512",
                "source_sha256": kernel_source_hash(),
                "calibration": {"kernel": cname.split("(")[0], "bytes_each_way": CALIB_BYTES,
-                               "fetch_kib": fetch[cname], "write_kib": write[cname],
+                               "fetch_kib": cal_fetch, "write_kib": cal_write,
                                "fetch_factor": f_fetch, "write_factor": f_write},
                "kernels": kernels,
                "commands": [
@@ -161,7 +190,7 @@ def summarize_pmc(fetch_dir, write_dir, replay):
                    "--no-cpu-baseline --no-graph --steps 5 --warmup 2 --cold-reps 0 --calib-copy",
                    "(same with WRITE_SIZE into $ROOT/gpurun_out/pmc_write)",
                    f"python bench.py --summarize-pmc gpurun_out/pmc_fetch gpurun_out/pmc_write"]}
-    path = TRAFFIC_FILE.format(r=replay)
+    path = out_path or TRAFFIC_FILE.format(r=replay)
     with open(path, "w") as f:
         json.dump(summary, f, indent=1)
     print(json.dumps(summary, indent=1))
@@ -186,7 +215,7 @@ def load_traffic(replay, kernel_short):
 def main():
     args = parse()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, args.replay)
+        summarize_pmc(*args.summarize_pmc, args.replay, args.pmc_out, args.pmc_workload)
         return
     if args.sweep:
         sweep(args)
@@ -519,95 +548,110 @@ def sweep(args):
     def emit(rec):
         print(json.dumps(rec), flush=True)
 
+    want = lambda name: not args.only or name in args.only.split(",")
+
     # ---- small fp32 layer (Hk = Hv = 4, d = 64): tail 205 + suffix 256
-    shape, hits = workloads.workload0()
-    h = hits[0]
-    xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
-    wst, st, _ = buffers(xt, 1, 4, 4, 64, False)
-    wsf, st2, o = buffers(xs, 1, 4, 4, 64, True)
-    wsr = fused_ws(xt, xs, 1, 4, 4, 64)
-    rep = timed_us(lambda: replay(xt, st, wst))
-    two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
-    both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
-    emit({"workload": "small fp32 layer Hk=Hv=4 d=64: tail 205 + suffix 256",
-          "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
-          "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
+    if want("small"):
+        shape, hits = workloads.workload0()
+        h = hits[0]
+        xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
+        wst, st, _ = buffers(xt, 1, 4, 4, 64, False)
+        wsf, st2, o = buffers(xs, 1, 4, 4, 64, True)
+        wsr = fused_ws(xt, xs, 1, 4, 4, 64)
+        rep = timed_us(lambda: replay(xt, st, wst))
+        two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+        both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
+        emit({"workload": "small fp32 layer Hk=Hv=4 d=64: tail 205 + suffix 256",
+              "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+              "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
 
     # ---- hybrid-model layer, tail 410 (the default bench line covers 819)
-    shape, hits = workloads.workload1(410)
-    h = hits[0]
-    xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
-    wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
-    wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
-    wsr = fused_ws(xt, xs, 1, 16, 32, 128)
-    rep = timed_us(lambda: replay(xt, st, wst))
-    two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
-    both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
-    emit({"workload": "one GDN layer Hk=16 Hv=32 d=128 bf16: tail 410 + suffix 512",
-          "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
-          "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
+    if want("layer410"):
+        shape, hits = workloads.workload1(410)
+        h = hits[0]
+        xt, xs = packed_dev(synth.pack([h.tail(shape)]), shape), packed_dev(synth.pack([h.suffix(shape)]), shape)
+        wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
+        wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
+        wsr = fused_ws(xt, xs, 1, 16, 32, 128)
+        rep = timed_us(lambda: replay(xt, st, wst))
+        two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+        both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
+        emit({"workload": "one GDN layer Hk=16 Hv=32 d=128 bf16: tail 410 + suffix 512",
+              "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+              "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
 
     # ---- 36-layer stack, m = 32768, r = 3277: 36 sequential per-layer replays,
     #      and the batched variant (layers as 36 sequences of one launch)
-    L, r2 = 36, 3277
-    xl = [random_dev([r2], 16, 32, 128, seed=100 + l) for l in range(L)]
-    wsl, stl, _ = buffers(xl[0], 1, 16, 32, 128, False)
-    seq = timed_us(lambda: [replay(x, stl, wsl) for x in xl])
-    xb = random_dev([r2] * L, 16, 32, 128, seed=7)
-    wsb, stb, _ = buffers(xb, L, 16, 32, 128, False)
-    bat = timed_us(lambda: replay(xb, stb, wsb))
-    emit({"workload": "36-layer stack Hk=16 Hv=32 d=128 bf16, m=32768, tail 3277 per layer",
-          "rebuild_latency_sequential_us": seq, "rebuild_latency_batched_us": bat,
-          "replay_tokens_per_s_sequential": L * r2 / (seq["p50"] * 1e-6),
-          "replay_tokens_per_s_batched": L * r2 / (bat["p50"] * 1e-6)})
+    if want("stack"):
+        L, r2 = 36, 3277
+        xl = [random_dev([r2], 16, 32, 128, seed=100 + l) for l in range(L)]
+        wsl, stl, _ = buffers(xl[0], 1, 16, 32, 128, False)
+        seq = timed_us(lambda: [replay(x, stl, wsl) for x in xl])
+        xb = random_dev([r2] * L, 16, 32, 128, seed=7)
+        wsb, stb, _ = buffers(xb, L, 16, 32, 128, False)
+        bat = timed_us(lambda: replay(xb, stb, wsb))
+        emit({"workload": "36-layer stack Hk=16 Hv=32 d=128 bf16, m=32768, tail 3277 per layer",
+              "rebuild_latency_sequential_us": seq, "rebuild_latency_batched_us": bat,
+              "replay_tokens_per_s_sequential": L * r2 / (seq["p50"] * 1e-6),
+              "replay_tokens_per_s_batched": L * r2 / (bat["p50"] * 1e-6)})
 
     # ---- 16 concurrent hits (varlen), one replay launch + one forward launch
-    draw = workloads.workload3_draw()
-    rl = [gdn.replay_len(m, ratio) for m, ratio, _ in draw]
-    shape, hits = workloads.workload3(rl)
-    xt = packed_dev(synth.pack([h.tail(shape) for h in hits]), shape)
-    xs = packed_dev(synth.pack([h.suffix(shape) for h in hits]), shape)
-    n = len(hits)
-    wst, st, _ = buffers(xt, n, 16, 32, 128, False)
-    wsf, st2, o = buffers(xs, n, 16, 32, 128, True)
-    wsr = fused_ws(xt, xs, n, 16, 32, 128)
-    rep = timed_us(lambda: replay(xt, st, wst))
-    two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
-    both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
-    sr, ss = sum(h.r for h in hits), sum(h.s for h in hits)
-    emit({"workload": f"16 varlen hits Hk=16 Hv=32 d=128 bf16: sum r={sr}, sum s={ss}",
-          "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
-          "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
-          "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
+    if want("hits"):
+        draw = workloads.workload3_draw()
+        rl = [gdn.replay_len(m, ratio) for m, ratio, _ in draw]
+        shape, hits = workloads.workload3(rl)
+        xt = packed_dev(synth.pack([h.tail(shape) for h in hits]), shape)
+        xs = packed_dev(synth.pack([h.suffix(shape) for h in hits]), shape)
+        n = len(hits)
+        wst, st, _ = buffers(xt, n, 16, 32, 128, False)
+        wsf, st2, o = buffers(xs, n, 16, 32, 128, True)
+        wsr = fused_ws(xt, xs, n, 16, 32, 128)
+        rep = timed_us(lambda: replay(xt, st, wst))
+        two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
+        both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
+        sr, ss = sum(h.r for h in hits), sum(h.s for h in hits)
+        emit({"workload": f"16 varlen hits Hk=16 Hv=32 d=128 bf16: sum r={sr}, sum s={ss}",
+              "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+              "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
+              "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
 
     # ---- decode steps after the rebuild: one token per sequence from the state,
     #      state updated in place; HBM-bound (the state is read and written once,
     #      with streaming loads and stores).  Timed as a HIP graph of 20 launches
     #      (no host overhead per step); the 1-sequence line is the first token's
     #      latency after a hit, the others are batched decode throughput.
-    for nb in (1, 64, 256):
-        xd = random_dev([1] * nb, 16, 32, 128, seed=900 + nb)
-        sd = torch.randn((nb, 32, 128, 128), dtype=torch.float32, device=dev) * 0.1
-        od = torch.empty((nb, 32, 128), dtype=torch.bfloat16, device=dev)
-        calls = 20
-        dec = lambda: [gdn.decode_step(xd["q"], xd["k"], xd["v"], xd["g"], xd["beta"], state_in=sd,
-                                       state_out=sd, o=od, scale=128 ** -0.5) for _ in range(calls)]
-        side = torch.cuda.Stream()
-        side.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(side):
-            dec()
-        torch.cuda.current_stream().wait_stream(side)
-        graph = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(graph):
-            dec()
-        t = timed_us(graph.replay)
-        per = t["p50"] / calls
-        nbytes = (2 * nb * 32 * 128 * 128 * 4 + 2 * nb * 16 * 128 * 2 + 2 * nb * 32 * 128 * 2
-                  + 2 * nb * 32 * 4)
-        emit({"workload": f"decode step Hk=16 Hv=32 d=128 bf16, {nb} sequences, state in place",
-              "us_per_step": per, "tokens_per_s": nb / (per * 1e-6),
-              "gbs": nbytes / (per * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (per * 1e-6) / 1e9 / HBM_PEAK_GBS,
-              "note": f"graph of {calls} launches per timed rep"})
+    if want("decode"):
+        if args.calib_copy:
+            # the PMC calibration kernel, as in the default run
+            src = torch.ones(CALIB_BYTES // 4, dtype=torch.float32, device=dev)
+            dst = torch.empty_like(src)
+            for _ in range(3):
+                torch.neg(src, out=dst)
+            torch.cuda.synchronize()
+            del src, dst
+        for nb in (int(x) for x in args.decode_seqs.split(",")):
+            xd = random_dev([1] * nb, 16, 32, 128, seed=900 + nb)
+            sd = torch.randn((nb, 32, 128, 128), dtype=torch.float32, device=dev) * 0.1
+            od = torch.empty((nb, 32, 128), dtype=torch.bfloat16, device=dev)
+            calls = 20
+            dec = lambda: [gdn.decode_step(xd["q"], xd["k"], xd["v"], xd["g"], xd["beta"], state_in=sd,
+                                           state_out=sd, o=od, scale=128 ** -0.5) for _ in range(calls)]
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                dec()
+            torch.cuda.current_stream().wait_stream(side)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                dec()
+            t = timed_us(graph.replay)
+            per = t["p50"] / calls
+            nbytes = (2 * nb * 32 * 128 * 128 * 4 + 2 * nb * 16 * 128 * 2 + 2 * nb * 32 * 128 * 2
+                      + 2 * nb * 32 * 4)
+            emit({"workload": f"decode step Hk=16 Hv=32 d=128 bf16, {nb} sequences, state in place",
+                  "us_per_step": per, "tokens_per_s": nb / (per * 1e-6),
+                  "gbs": nbytes / (per * 1e-6) / 1e9, "frac_of_hbm_peak": nbytes / (per * 1e-6) / 1e9 / HBM_PEAK_GBS,
+                  "note": f"graph of {calls} launches per timed rep"})
 
     # ---- FA-KV transfer overlapped with the replay (paper Section 3, "Replay
     #      efficiency"): a hit of m tokens moves the full-attention KV of the
@@ -617,81 +661,83 @@ def sweep(args):
     #      (Hk=16, Hv=32, d=128) and 32 KiB of FA KV per token (8 FA layers x
     #      K, V x 4 KV heads x 256 x bf16).  H2D-SER: copy, replays, forwards on
     #      one stream; H2D-OVL: copy on a second stream beside the replays.
-    n_la, kv_per_token = 24, 32 << 10
-    copy_stream = torch.cuda.Stream()
-    for m in (8192, 32768):
-        r = {8192: 819, 32768: 3277}[m]
-        host_kv = torch.empty(m * kv_per_token, dtype=torch.uint8, pin_memory=True)
-        dev_kv = torch.empty(m * kv_per_token, dtype=torch.uint8, device=dev)
-        xl = [random_dev([r], 16, 32, 128, seed=2000 + l) for l in range(n_la)]
-        xq = [random_dev([512], 16, 32, 128, seed=3000 + l) for l in range(n_la)]
-        wst, st, _ = buffers(xl[0], 1, 16, 32, 128, False)
-        wsf, st2, o = buffers(xq[0], 1, 16, 32, 128, True)
+    if want("h2d"):
+        n_la, kv_per_token = 24, 32 << 10
+        copy_stream = torch.cuda.Stream()
+        for m in (8192, 32768):
+            r = {8192: 819, 32768: 3277}[m]
+            host_kv = torch.empty(m * kv_per_token, dtype=torch.uint8, pin_memory=True)
+            dev_kv = torch.empty(m * kv_per_token, dtype=torch.uint8, device=dev)
+            xl = [random_dev([r], 16, 32, 128, seed=2000 + l) for l in range(n_la)]
+            xq = [random_dev([512], 16, 32, 128, seed=3000 + l) for l in range(n_la)]
+            wst, st, _ = buffers(xl[0], 1, 16, 32, 128, False)
+            wsf, st2, o = buffers(xq[0], 1, 16, 32, 128, True)
 
-        def replays():
-            for x in xl:
-                replay(x, st, wst)
+            def replays():
+                for x in xl:
+                    replay(x, st, wst)
 
-        def forwards():
-            for x in xq:
-                forward(x, st, o, st2, wsf)
+            def forwards():
+                for x in xq:
+                    forward(x, st, o, st2, wsf)
 
-        def h2d(stream):
-            with torch.cuda.stream(stream):
-                dev_kv.copy_(host_kv, non_blocking=True)
+            def h2d(stream):
+                with torch.cuda.stream(stream):
+                    dev_kv.copy_(host_kv, non_blocking=True)
 
-        main = torch.cuda.current_stream()
+            main = torch.cuda.current_stream()
 
-        def serial():
-            h2d(main)
-            replays()
-            forwards()
+            def serial():
+                h2d(main)
+                replays()
+                forwards()
 
-        def overlapped():
-            copy_stream.wait_stream(main)
-            h2d(copy_stream)
-            replays()
-            main.wait_stream(copy_stream)
-            forwards()
+            def overlapped():
+                copy_stream.wait_stream(main)
+                h2d(copy_stream)
+                replays()
+                main.wait_stream(copy_stream)
+                forwards()
 
-        t_h2d = timed_us(lambda: h2d(main))
-        t_rep = timed_us(replays)
-        t_fwd = timed_us(forwards)
-        t_ser = timed_us(serial)
-        t_ovl = timed_us(overlapped)
-        hidden = (t_ser["p50"] - t_ovl["p50"]) / min(t_h2d["p50"], t_rep["p50"])
-        emit({"workload": f"FA-KV H2D overlapped with replay, m={m}, r={r}, {n_la} GDN layers, "
-                          f"{m * kv_per_token >> 20} MiB FA KV, suffix 512",
-              "h2d_us": t_h2d["p50"], "h2d_gbs": m * kv_per_token / (t_h2d["p50"] * 1e-6) / 1e9,
-              "replay_us": t_rep["p50"], "suffix_forward_us": t_fwd["p50"],
-              "h2d_ser_us": t_ser["p50"], "h2d_ovl_us": t_ovl["p50"],
-              "ovl_vs_ser_reduction": 1 - t_ovl["p50"] / t_ser["p50"],
-              "hidden_fraction_of_shorter": hidden})
-        del host_kv, dev_kv, xl, xq
+            t_h2d = timed_us(lambda: h2d(main))
+            t_rep = timed_us(replays)
+            t_fwd = timed_us(forwards)
+            t_ser = timed_us(serial)
+            t_ovl = timed_us(overlapped)
+            hidden = (t_ser["p50"] - t_ovl["p50"]) / min(t_h2d["p50"], t_rep["p50"])
+            emit({"workload": f"FA-KV H2D overlapped with replay, m={m}, r={r}, {n_la} GDN layers, "
+                              f"{m * kv_per_token >> 20} MiB FA KV, suffix 512",
+                  "h2d_us": t_h2d["p50"], "h2d_gbs": m * kv_per_token / (t_h2d["p50"] * 1e-6) / 1e9,
+                  "replay_us": t_rep["p50"], "suffix_forward_us": t_fwd["p50"],
+                  "h2d_ser_us": t_ser["p50"], "h2d_ovl_us": t_ovl["p50"],
+                  "ovl_vs_ser_reduction": 1 - t_ovl["p50"] / t_ser["p50"],
+                  "hidden_fraction_of_shorter": hidden})
+            del host_kv, dev_kv, xl, xq
 
     # ---- replay vs full prefill, suffix 512: t_full = forward(0, m + s) with
     #      outputs; t_replay = the fused replay(r) + forward(S_m, s); state-only
     #      full = replay(m + s)
-    for m in (8192, 16384, 32768):
-        x_full = random_dev([m + 512], 16, 32, 128, seed=m)
-        wsF, stF, oF = buffers(x_full, 1, 16, 32, 128, True)
-        wsR, stR, _ = buffers(x_full, 1, 16, 32, 128, False)
-        t_full = timed_us(lambda: forward(x_full, None, oF, stF, wsF))
-        t_state = timed_us(lambda: replay(x_full, stR, wsR))
-        for pct in ("0.05", "0.1"):
-            # the configs' integers where they round to nearest, else the paper's ceiling
-            r = {(8192, "0.1"): 819, (32768, "0.05"): 1638}.get((m, pct), gdn.replay_len(m, pct))
-            xt = random_dev([r], 16, 32, 128, seed=m + r)
-            xs = random_dev([512], 16, 32, 128, seed=m + 1)
-            st = torch.empty((1, 32, 128, 128), dtype=torch.float32, device=dev)
-            st2 = torch.empty_like(st)
-            o = torch.empty((512, 32, 128), dtype=torch.bfloat16, device=dev)
-            wsr = fused_ws(xt, xs, 1, 16, 32, 128)
-            t_rep = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
-            emit({"workload": f"replay vs full prefill Hk=16 Hv=32 d=128 bf16, m={m}, r={r}, suffix 512",
-                  "t_full_us": t_full["p50"], "t_full_state_only_us": t_state["p50"],
-                  "t_replay_us": t_rep["p50"], "speedup": t_full["p50"] / t_rep["p50"],
-                  "speedup_state_only_full": t_state["p50"] / t_rep["p50"]})
+    if want("full"):
+        for m in (8192, 16384, 32768):
+            x_full = random_dev([m + 512], 16, 32, 128, seed=m)
+            wsF, stF, oF = buffers(x_full, 1, 16, 32, 128, True)
+            wsR, stR, _ = buffers(x_full, 1, 16, 32, 128, False)
+            t_full = timed_us(lambda: forward(x_full, None, oF, stF, wsF))
+            t_state = timed_us(lambda: replay(x_full, stR, wsR))
+            for pct in ("0.05", "0.1"):
+                # the configs' integers where they round to nearest, else the paper's ceiling
+                r = {(8192, "0.1"): 819, (32768, "0.05"): 1638}.get((m, pct), gdn.replay_len(m, pct))
+                xt = random_dev([r], 16, 32, 128, seed=m + r)
+                xs = random_dev([512], 16, 32, 128, seed=m + 1)
+                st = torch.empty((1, 32, 128, 128), dtype=torch.float32, device=dev)
+                st2 = torch.empty_like(st)
+                o = torch.empty((512, 32, 128), dtype=torch.bfloat16, device=dev)
+                wsr = fused_ws(xt, xs, 1, 16, 32, 128)
+                t_rep = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
+                emit({"workload": f"replay vs full prefill Hk=16 Hv=32 d=128 bf16, m={m}, r={r}, suffix 512",
+                      "t_full_us": t_full["p50"], "t_full_state_only_us": t_state["p50"],
+                      "t_replay_us": t_rep["p50"], "speedup": t_full["p50"] / t_rep["p50"],
+                      "speedup_state_only_full": t_state["p50"] / t_rep["p50"]})
 
 
 def cpu_baseline(tail, suf, r, s, seconds):
