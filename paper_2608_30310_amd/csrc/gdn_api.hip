@@ -34,8 +34,9 @@ namespace {
 thread_local std::string t_last_error;
 
 constexpr int kThreads = 256;
-// grid limits in make_plan assume <= 1024 work items per (sequence, head) in any grid dimension
-static_assert(kThreads <= 256 && cols_threads(true) <= 256 && head_threads(128) <= 1024, "grid limits");
+// grid limits in make_plan assume <= 1024 work items per (sequence, head) in any
+// grid dimension; the column-split scan's grid is bounded by the CU count instead
+static_assert(kThreads <= 256 && kDecodeThreads <= 1024 && head_threads(128) <= 1024, "grid limits");
 
 // ------------------------------------------------------------ host side
 gdn_status fail(gdn_status st, const std::string& msg) {
@@ -124,7 +125,7 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
   gdn_status st = cols_fit(s, &fits, &col_groups);
   if (st != GDN_OK) return st;
   if (fits) {
-    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD)), 0, stream, cu,
+    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0, stream, cu,
                        s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, Pw,
                        state_in, static_cast<TIn*>(o), state_out);
   } else {

@@ -27,6 +27,8 @@
 #include "gdn_intra.h"
 #include "gdn_plan.h"
 
+#include <type_traits>
+
 namespace gdn {
 
 constexpr int kLdsBytes = 160 * 1024;
@@ -456,10 +458,14 @@ __device__ __forceinline__ void store_chunk_out(TIn* o, const ScanUnit& u, int c
 // the chip at once, where per-chunk latency is all that matters.  Tail replay:
 // two compute waves (16 columns each) and one wave that only issues DMA.  With
 // outputs: the two waves that carry the recurrence hand Delta and the split
-// state to two output waves (one per 16 columns), which also issue the DMA,
-// so the outputs' products stay off the sequential chain.
+// state to two output waves (one per 16 columns), so the outputs' products
+// stay off the sequential chain, and a fifth wave issues the DMA.
 constexpr int kColsPerGroup = 32;
-constexpr int cols_threads(bool fwd) { return (fwd ? 4 : 3) * kWave; }
+// With outputs, bf16 inputs get a dedicated DMA wave; for fp32 inputs the
+// recurrence wave needs ~250 VGPRs, more than two waves sharing a SIMD may
+// hold, so the two output waves issue the DMA instead (4 waves).
+constexpr bool cols_dma_wave(bool fwd, bool split) { return fwd && !split; }
+constexpr int cols_threads(bool fwd, bool split) { return (fwd ? (split ? 4 : 5) : 3) * kWave; }
 
 template <typename TIn, int DK, bool FWD>
 using ColsLds = ScanLds<TIn, DK, kColsPerGroup, FWD, true>;
@@ -562,15 +568,20 @@ struct ColsOutLayout {
 };
 
 // One column-split workgroup with outputs (block `block` of `nblocks`), LDS in
-// `lds_l`.  Waves 0 and 1 carry the recurrence of columns 16 w.. (chunk_step
+// `lds_l`.  Two waves carry the recurrence of columns 16 c.. (chunk_step
 // without outputs, exporting Delta before its region 5 and the split of M1 at
-// its end); wave 2 + w writes the outputs of the same columns:
+// its end) and two write the outputs of the same columns:
 //   before the mid-chunk barrier: (Q M0)^T from the split M0 of the chunk;
 //   after it: O^T = diag-scaled (Q M0)^T + Delta^T P^T, stored at the start
 //   of the next chunk.
-// Waves 2 and 3 share the next chunk's DMA, half before and half after the
-// mid-chunk barrier.  The products are those of chunk_step with outputs, in
-// the same order, so the results are the same bit for bit.
+// With a DMA wave (bf16 inputs): wave 0 issues the next chunk's DMA (two
+// thirds before the mid-chunk barrier, the rest after it), waves 1 + c carry
+// the recurrence, waves 3 + c write the outputs; with waves assigned to SIMDs
+// in turn, the DMA wave shares a SIMD with an output wave and each recurrence
+// wave has one to itself.  Without (fp32 inputs): waves c carry the
+// recurrence, waves 2 + c write the outputs and each issues half of the DMA.
+// The products are those of chunk_step with outputs, in the same order, so the
+// results are the same bit for bit.
 template <typename TIn, int DK>
 __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, int nblocks,
                                                    const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
@@ -585,14 +596,19 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   constexpr int NT = DK / 16, NK = DK / 32;
   constexpr int NKA = ka_frags(DK), NKT = kt_frags(DK);
   constexpr int NKF = L::kKFrags;
-  static_assert(L::kKJobs % 2 == 0 && L::kTJobs % 2 == 0 && L::kPJobs == 0 && L::kVJobs % 2 == 0,
-                "DMA halves need records of whole multiples of 2 KiB");
+  constexpr bool DMA_WAVE = cols_dma_wave(true, SPLIT);
+  constexpr int kEarlyJobs = 2 * L::kJobs / 3;   // DMA jobs issued before the mid-chunk barrier
+  static_assert(DMA_WAVE || (L::kKJobs % 2 == 0 && L::kTJobs % 2 == 0 && L::kPJobs == 0 &&
+                             L::kVJobs % 2 == 0), "DMA halves need records of whole multiples of 2 KiB");
   constexpr int kHalf = (L::kKJobs + L::kTJobs + L::kVJobs) / 2;   // jobs per output wave, scalars aside
   const int tid = threadIdx.x;
   // wave index made provably uniform: DMA destinations (M0) stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const bool out_wave = wave >= 2;
-  const int tile = wave & 1, h = wave & 1;
+  const int first_chain = DMA_WAVE ? 1 : 0;
+  const bool dma_wave = DMA_WAVE && wave == 0;
+  const bool chain_wave = wave == first_chain || wave == first_chain + 1;
+  const bool out_wave = wave >= first_chain + 2;
+  const int tile = (wave - first_chain) & 1, h = tile;
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
   const int ngroups = dv / kColsPerGroup;
   // logical unit: the column groups of a value head, then the value heads of a
@@ -605,9 +621,21 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   unsigned char* xd = (unsigned char*)(lds_l + CL::kOffX + tile * CL::kTileBytes);
   unsigned char* xm = xd + CL::kDBytes;
 
-  // jobs 2 q + h of the K record, the T record and the V rows for q in
-  // [q0, q1) (every record is a multiple of two jobs, so which record a job
-  // reads is known at compile time); the scalars with the second half
+  // DMA jobs [j0, j1) of chunk ci into buffer b (the job index is a
+  // compile-time constant in each instance, so every job is straight code)
+  auto dma_jobs = [&](int ci, int b, auto j0c, auto j1c) __attribute__((always_inline)) {
+    constexpr int j0 = decltype(j0c)::value, j1 = decltype(j1c)::value;
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
+#pragma unroll
+    for (int j = j0; j < j1; ++j) dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
+  };
+  using J0 = std::integral_constant<int, 0>;
+  using JE = std::integral_constant<int, kEarlyJobs>;
+  using JN = std::integral_constant<int, L::kJobs>;
+  // without a DMA wave: jobs 2 q + h of the K record, the T record and the V
+  // rows for q in [q0, q1) (every record is a multiple of two jobs, so which
+  // record a job reads is known at compile time); the scalars with the
+  // second half
   auto dma_half = [&](int ci, int b, int q0, int q1) __attribute__((always_inline)) {
     const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
     lds_byte* dst = lds_l + b * L::kBytes;
@@ -635,7 +663,7 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   Frag mb[NK];
   f32x4 pout[4];
   const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * dv + colw + lr;
-  if (!out_wave) {
+  if (chain_wave) {
     load_state<DK>(state_in, sbase, dv, lg, M, mb);
     u32x4* x = reinterpret_cast<u32x4*>(xm);
 #pragma unroll
@@ -644,46 +672,55 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
       x[(2 * kk + 1) * kWave + lane] = __builtin_bit_cast(u32x4, mb[kk].lo);
     }
   } else if (u.nch > 0) {
-    dma_half(0, 0, 0, kHalf);
-    wait_dma();
+    if (dma_wave) {
+      dma_jobs(0, 0, J0{}, JN{});
+      wait_dma();
+    } else if (!DMA_WAVE) {
+      dma_half(0, 0, 0, kHalf);
+      wait_dma();
+    }
   }
   __syncthreads();
   for (int ci = 0; ci < u.nch; ++ci) {
     const int b = CL::kBuffers == 2 ? (ci & 1) : 0;
     const unsigned char* base = (const unsigned char*)(lds_l + b * L::kBytes);
     const bool prefetch = CL::kBuffers == 2 && ci + 1 < u.nch;
-    if (!out_wave) {
+    if (chain_wave) {
       chunk_step<L, DK, false, true>(base, 16 * tile, nullptr, lane, M, mb, pout,
                                      [](int k) __attribute__((always_inline)) {
                                        if (k == 5) lds_barrier();   // Delta is out
                                      },
                                      xd, xm);
+    } else if (dma_wave) {
+      if (prefetch) dma_jobs(ci + 1, b ^ 1, J0{}, JE{});
+      lds_barrier();
+      if (prefetch) dma_jobs(ci + 1, b ^ 1, JE{}, JN{});
     } else {
       if (ci > 0) store_chunk_out(o, u, ci - 1, hv, dv, colw, lane, pout);
-      if (prefetch) dma_half(ci + 1, b ^ 1, 0, kHalf / 2);
+      if (!DMA_WAVE && prefetch) dma_half(ci + 1, b ^ 1, 0, kHalf / 2);
       // (Q M0)^T: A = split M0 from the recurrence wave, B = Q fragments
       const u32x4* kf = reinterpret_cast<const u32x4*>(base + L::kOffK);
       const u32x4* x = reinterpret_cast<const u32x4*>(xm);
-      Frag m0[NK], qa[4][NK];
+      Frag m0[NK];
 #pragma unroll
       for (int kk = 0; kk < NK; ++kk) {
         m0[kk].hi = __builtin_bit_cast(bf16x8, x[(2 * kk) * kWave + lane]);
         m0[kk].lo = __builtin_bit_cast(bf16x8, x[(2 * kk + 1) * kWave + lane]);
       }
-#pragma unroll
-      for (int ti = 0; ti < 4; ++ti)
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
-          const int f = NKA + NKT + ti * NK + kk;
-          qa[ti][kk].hi = __builtin_bit_cast(bf16x8, kf[f * kWave + lane]);
-          if constexpr (SPLIT) qa[ti][kk].lo = __builtin_bit_cast(bf16x8, kf[(NKF + f) * kWave + lane]);
-        }
+      // one token tile's Q fragments at a time (fp32 inputs carry hi and lo)
       f32x4 qm[4];
 #pragma unroll
       for (int ti = 0; ti < 4; ++ti) {
+        Frag qa[NK];
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+          const int f = NKA + NKT + ti * NK + kk;
+          qa[kk].hi = __builtin_bit_cast(bf16x8, kf[f * kWave + lane]);
+          if constexpr (SPLIT) qa[kk].lo = __builtin_bit_cast(bf16x8, kf[(NKF + f) * kWave + lane]);
+        }
         qm[ti] = zero4();
 #pragma unroll
-        for (int kk = 0; kk < NK; ++kk) qm[ti] = mma_b<SPLIT>(m0[kk], qa[ti][kk], qm[ti]);
+        for (int kk = 0; kk < NK; ++kk) qm[ti] = mma_b<SPLIT>(m0[kk], qa[kk], qm[ti]);
       }
       // P (split, six nonzero fragments) from global memory
       const u32x4* pg = Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave);
@@ -709,18 +746,21 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
         pout[ti] = mma_x3(dd0, pfr[tri_frag(ti, 0)], pout[ti]);
         if (ti >= 2) pout[ti] = mma_x3(dd1, pfr[tri_frag(ti, 1)], pout[ti]);
       }
-      if (prefetch) dma_half(ci + 1, b ^ 1, kHalf / 2, kHalf);
+      if (!DMA_WAVE && prefetch) dma_half(ci + 1, b ^ 1, kHalf / 2, kHalf);
     }
     if (CL::kBuffers == 1) {
       __syncthreads();   // every wave is done with the only buffer
-      if (out_wave && ci + 1 < u.nch) dma_half(ci + 1, 0, 0, kHalf);
+      if (ci + 1 < u.nch) {
+        if (dma_wave) dma_jobs(ci + 1, 0, J0{}, JN{});
+        else if (!DMA_WAVE && out_wave) dma_half(ci + 1, 0, 0, kHalf);
+      }
     }
-    if (out_wave) wait_dma();
+    if (dma_wave || (!DMA_WAVE && out_wave)) wait_dma();
     __syncthreads();     // next chunk's operands are in LDS; this buffer is free
   }
   if (out_wave) {
     if (u.nch > 0) store_chunk_out(o, u, u.nch - 1, hv, dv, colw, lane, pout);
-  } else if (state_out) {
+  } else if (chain_wave && state_out) {
 #pragma unroll
     for (int td = 0; td < NT; ++td)
 #pragma unroll
@@ -730,7 +770,7 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
 }
 
 template <typename TIn, int DK, bool FWD>
-__global__ __launch_bounds__(cols_threads(FWD)) __attribute__((amdgpu_waves_per_eu(1, 1)))
+__global__ __launch_bounds__(cols_threads(FWD, sizeof(TIn) == 4)) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
                  const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                  const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
