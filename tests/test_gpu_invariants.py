@@ -189,19 +189,24 @@ def test_whole_head_and_column_kernels_agree():
         assert rel.item() <= 1e-3   # bf16 outputs: one rounding step apart at most
 
 
-@pytest.mark.parametrize("case", ["one", "ragged", "wide"])
+@pytest.mark.parametrize("case", ["one", "ragged", "wide", "ragged_d64", "ragged_dk64", "ragged_dv64"])
 def test_replay_forward_equals_the_two_calls_bitwise(case):
     # the fused call runs the same kernels (the suffix's chunk preparation
     # beside the tail scan), so it must reproduce tail_replay + chunk_forward
+    # "ragged*" covers an empty tail and an empty suffix at every (d_k, d_v)
+    # the kernels are built for; "wide" runs the whole-head scan kernel
+    shape = {"ragged_d64": synth.Shape(hk=2, hv=4, dk=64, dv=64, dtype="bf16"),
+             "ragged_dk64": synth.Shape(hk=2, hv=4, dk=64, dv=128, dtype="bf16"),
+             "ragged_dv64": synth.Shape(hk=2, hv=4, dk=128, dv=64, dtype="bf16")}.get(case, SHAPE)
     if case == "one":
         rs, ss = [333], [200]
-    elif case == "ragged":
+    elif case.startswith("ragged"):
         rs, ss = [0, 1, 64, 130, 257], [65, 0, 1, 200, 64]
     else:   # enough heads that the whole-head scan kernel runs
         rs = [1 + (37 * i) % 150 for i in range(72)]
         ss = [1 + (53 * i) % 120 for i in range(72)]
-    tails = synth.pack([_seq(i, r, start=0) for i, r in enumerate(rs)])
-    sufs = synth.pack([_seq(i, s, start=r) for i, (r, s) in enumerate(zip(rs, ss))])
+    tails = synth.pack([_seq(i, r, start=0, shape=shape) for i, r in enumerate(rs)])
+    sufs = synth.pack([_seq(i, s, start=r, shape=shape) for i, (r, s) in enumerate(zip(rs, ss))])
     xt, xs = device_inputs(tails), device_inputs(sufs)
     st = gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"])
     o, st2 = gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"],
