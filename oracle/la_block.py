@@ -8,8 +8,8 @@ is written out here as the usual Gated DeltaNet layer, every step in plain
 NumPy on one packed batch of sequences, with the recurrence itself from the
 compiled oracle (``oracle.recurrence``, Eq. 1 and Eq. 2):
 
-1. in-projection   P = X W_in, columns [q | k | v | z | a | b]
-                   (Hk d_k, Hk d_k, Hv d_v, Hv d_v, Hv, Hv);
+1. in-projection   P = X W_in^T, columns [q | k | v | a | b | z]
+                   (Hk d_k, Hk d_k, Hv d_v, Hv, Hv, Hv d_v);
 2. short causal depthwise convolution over the q, k, v channels, K taps,
                    c[t] = sum_j w[:, j] u[t - (K - 1) + j], with u = 0 before
                    each sequence's first token (the conv history restarts with
@@ -19,11 +19,15 @@ compiled oracle (``oracle.recurrence``, Eq. 1 and Eq. 2):
 5. the recurrence from the zero state, o_t = scale S_t q_t;
 6. gated RMS norm per (token, head): y = o / sqrt(mean(o^2) + eps) * w_norm
                    * silu(z);
-7. out-projection  out = Y W_out.
+7. out-projection  out = Y W_out^T.
 
-Layouts (float64): X [T, D]; W_in [D, 2 Hk d_k + 2 Hv d_v + 2 Hv];
+Layouts (float64; the two projections as linear layers store them,
+[out_features, in_features]): X [T, D]; W_in [2 Hk d_k + 2 Hv d_v + 2 Hv, D];
 conv_w [2 Hk d_k + Hv d_v, K]; A_log, dt_bias [Hv]; w_norm [d_v];
-W_out [Hv d_v, D]; state [N, Hv, d_k, d_v] (M = S^T); out [T, D].
+W_out [D, Hv d_v]; state [N, Hv, d_k, d_v] (M = S^T); out [T, D].
+The column order puts everything the state needs (k, v, a, b) in one
+contiguous block, so a state-only replay projects onto rows cq .. of W_in
+alone.
 """
 from __future__ import annotations
 
@@ -92,11 +96,11 @@ def la_block(x, w_in, conv_w, a_log, dt_bias, w_norm, w_out, cu_seqlens, hk, hv,
     x = np.asarray(x, np.float64)
     T = x.shape[0]
     cq, cv = hk * dk, hv * dv
-    P = x @ np.asarray(w_in, np.float64)
+    P = x @ np.asarray(w_in, np.float64).T
     u = P[:, :2 * cq + cv]
-    z = P[:, 2 * cq + cv:2 * cq + 2 * cv]
-    a = P[:, 2 * cq + 2 * cv:2 * cq + 2 * cv + hv]
-    b = P[:, 2 * cq + 2 * cv + hv:]
+    a = P[:, 2 * cq + cv:2 * cq + cv + hv]
+    b = P[:, 2 * cq + cv + hv:2 * cq + cv + 2 * hv]
+    z = P[:, 2 * cq + cv + 2 * hv:]
     c = silu(causal_conv(u, conv_w, cu_seqlens))
     q = c[:, :cq].reshape(T, hk, dk)
     k = c[:, cq:2 * cq].reshape(T, hk, dk)
@@ -110,5 +114,5 @@ def la_block(x, w_in, conv_w, a_log, dt_bias, w_norm, w_out, cu_seqlens, hk, hv,
         return state, None, parts
     y = gated_rmsnorm(o, z.reshape(T, hv, dv), w_norm, norm_eps)
     parts["y"] = y
-    out = y.reshape(T, cv) @ np.asarray(w_out, np.float64)
+    out = y.reshape(T, cv) @ np.asarray(w_out, np.float64).T
     return state, out, parts

@@ -11,7 +11,11 @@ independently of it (CPU only).
   * q and k come out with unit norm; g <= 0 and 0 < beta < 1;
   * the gated RMS norm removes any positive scale of o (o is linear in V
     from the zero state), with a worked case of exact decimals;
-  * the output is linear in W_out;
+  * the output is linear in W_out, and vanishes when the z rows of W_in do
+    (silu(0) = 0);
+  * which weights reach which result: the state ignores the q and z rows,
+    w_norm and W_out; beta ignores the a rows and g the b rows; the
+    state-only run gives the same state;
   * replaying a tail behind K - 1 zero tokens changes nothing (zero hiddens
     give zero keys and values, so the state stays zero and the convolution
     sees zeros either way): the reading that the conv history restarts with
@@ -28,11 +32,11 @@ HK, HV, DK, DV, D, K = 1, 2, 4, 3, 6, 4
 
 def _weights(rng, scale_v=1.0):
     cq, cv = HK * DK, HV * DV
-    w_in = rng.standard_normal((D, 2 * cq + 2 * cv + 2 * HV)) / np.sqrt(D)
-    w_in[:, 2 * cq:2 * cq + cv] *= scale_v
+    w_in = rng.standard_normal((2 * cq + 2 * cv + 2 * HV, D)) / np.sqrt(D)
+    w_in[2 * cq:2 * cq + cv] *= scale_v
     return dict(w_in=w_in, conv_w=rng.standard_normal((2 * cq + cv, K)) * 0.5,
                 a_log=rng.uniform(-1.0, 0.5, HV), dt_bias=rng.uniform(-1.0, 1.0, HV),
-                w_norm=rng.uniform(0.5, 1.5, DV), w_out=rng.standard_normal((HV * DV, D)) / np.sqrt(HV * DV))
+                w_norm=rng.uniform(0.5, 1.5, DV), w_out=rng.standard_normal((D, HV * DV)) / np.sqrt(HV * DV))
 
 
 def _run(x, w, cu, fn=None, **kw):
@@ -67,7 +71,7 @@ def pin_single_token(block):
     rng = np.random.default_rng(2)
     w = _weights(rng)
     cq, cv = HK * DK, HV * DV
-    w["w_in"][:, 2 * cq + 2 * cv:] = 0.0          # a = b = 0
+    w["w_in"][2 * cq + cv:2 * cq + cv + 2 * HV] = 0.0   # a = b = 0
     w["a_log"][:] = 0.0
     w["dt_bias"][:] = 0.0                          # g = -softplus(0) = -ln 2, beta = 1/2
     x = rng.standard_normal((1, D))
@@ -137,8 +141,58 @@ def pin_zero_prefix_changes_nothing(block):
     np.testing.assert_allclose(o2[K - 1:], o1, rtol=1e-12, atol=1e-15)
 
 
-BLOCK_PINS = [pin_single_token, pin_norms_and_gate_ranges, pin_gated_norm,
-              pin_out_is_linear_in_w_out, pin_zero_prefix_changes_nothing]
+def pin_zero_gate_silences_output(block):
+    """Zero rows of W_in for z give z = 0, silu(0) = 0, so y = 0 and out = 0
+    exactly, whatever the state does; zero rows for v give v = 0 and a zero
+    state."""
+    rng = np.random.default_rng(9)
+    w = _weights(rng)
+    cq, cv = HK * DK, HV * DV
+    w["w_in"][2 * cq + cv + 2 * HV:] = 0.0
+    x = rng.standard_normal((6, D))
+    s, out, _ = _run(x, w, np.array([0, 6]), block)
+    assert np.all(out == 0.0) and np.any(s != 0.0)
+    w = _weights(rng)
+    w["w_in"][2 * cq:2 * cq + cv] = 0.0
+    s, out, _ = _run(x, w, np.array([0, 6]), block)
+    assert np.all(s == 0.0)
+
+
+def pin_what_depends_on_what(block):
+    """Which weights reach which result: the state does not see the q or z
+    rows of W_in, w_norm or W_out; beta does not see the a rows, g not the b
+    rows; and the state-only run (outputs=False) gives the same state."""
+    rng = np.random.default_rng(10)
+    w = _weights(rng)
+    cq, cv = HK * DK, HV * DV
+    x = rng.standard_normal((10, D))
+    cu = np.array([0, 3, 10])
+    s0, _, p0 = _run(x, w, cu, block)
+    rows = dict(q=slice(0, cq), a=slice(2 * cq + cv, 2 * cq + cv + HV),
+                b=slice(2 * cq + cv + HV, 2 * cq + cv + 2 * HV), z=slice(2 * cq + cv + 2 * HV, None))
+    for name in ("q", "z"):
+        w1 = dict(w, w_in=w["w_in"].copy())
+        w1["w_in"][rows[name]] = rng.standard_normal(w1["w_in"][rows[name]].shape)
+        s1, _, _ = _run(x, w1, cu, block)
+        assert np.array_equal(s1, s0), name
+    w1 = dict(w, w_norm=2.0 * w["w_norm"], w_out=-w["w_out"])
+    s1, _, _ = _run(x, w1, cu, block)
+    assert np.array_equal(s1, s0)
+    for name, kept in (("a", "beta"), ("b", "g")):
+        w1 = dict(w, w_in=w["w_in"].copy())
+        w1["w_in"][rows[name]] += 1.0
+        _, _, p1 = _run(x, w1, cu, block)
+        assert np.array_equal(p1[kept], p0[kept]), name
+        other = "g" if kept == "beta" else "beta"
+        assert not np.allclose(p1[other], p0[other]), name
+    s2, out2, _ = _run(x, w, cu, block, outputs=False)
+    assert out2 is None
+    np.testing.assert_allclose(s2, s0, rtol=1e-13, atol=1e-15)
+
+
+BLOCK_PINS = [pin_what_depends_on_what, pin_single_token, pin_norms_and_gate_ranges, pin_gated_norm,
+              pin_out_is_linear_in_w_out, pin_zero_prefix_changes_nothing,
+              pin_zero_gate_silences_output]
 
 
 def test_conv_pin():
@@ -191,6 +245,18 @@ def _shifted_conv(u, w, cu):   # off by one token
     return out
 
 
+def _rows_read_as(order):
+    """The block reading W_in's row blocks in another order (a slicing mistake)."""
+    def block(x, w_in, *args, **kw):
+        cq, cv = HK * DK, HV * DV
+        spans = dict(q=(0, cq), k=(cq, 2 * cq), v=(2 * cq, 2 * cq + cv), a=(2 * cq + cv, 2 * cq + cv + HV),
+                     b=(2 * cq + cv + HV, 2 * cq + cv + 2 * HV), z=(2 * cq + cv + 2 * HV, 2 * cq + 2 * cv + 2 * HV))
+        # sizes follow the true order; contents come from `order`'s reading of the rows
+        flat = np.concatenate([w_in[slice(*spans[n])] for n in order])
+        return lb.la_block(x, flat, *args, **kw)
+    return block
+
+
 MUTANTS = {
     "conv taps not reversed": ("conv", _mutant_conv_unreversed),
     "conv history across sequences": ("conv", _mutant_conv_no_restart),
@@ -200,6 +266,8 @@ MUTANTS = {
     "silu as identity": ("block", _block_with(silu=lambda x: x)),
     "norm without the rms": ("block", _block_with(gated_rmsnorm=lambda o, z, w, e: o * w * lb.silu(z))),
     "l2 norm missing": ("block", _block_with(l2norm=lambda x, e: x)),
+    "a and b swapped": ("block", _rows_read_as("qkvbaz")),
+    "q and k swapped": ("block", _rows_read_as("kqvabz")),
 }
 
 
