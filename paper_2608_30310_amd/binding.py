@@ -37,6 +37,19 @@ class GDNShape(ctypes.Structure):
                 ("scale", ctypes.c_float)]
 
 
+class LAShape(ctypes.Structure):
+    _fields_ = [("num_seqs", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("num_k_heads", ctypes.c_int32), ("num_v_heads", ctypes.c_int32),
+                ("d_k", ctypes.c_int32), ("d_v", ctypes.c_int32), ("conv_taps", ctypes.c_int32),
+                ("act_dtype", ctypes.c_int32), ("scale", ctypes.c_float),
+                ("l2_eps", ctypes.c_float), ("norm_eps", ctypes.c_float)]
+
+
+class LAWeights(ctypes.Structure):
+    _fields_ = [("w_in", ctypes.c_void_p), ("conv_w", ctypes.c_void_p), ("a_log", ctypes.c_void_p),
+                ("dt_bias", ctypes.c_void_p), ("norm_w", ctypes.c_void_p), ("w_out", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -78,6 +91,18 @@ def load_library():
     lib.gdn_stage_name.restype = ctypes.c_char_p
     lib.gdn_decode_step.argtypes = [SP, P, P, P, P, P, P, P, P, P]
     lib.gdn_decode_step.restype = ctypes.c_int
+    LP = ctypes.POINTER(LAShape)
+    WP = ctypes.POINTER(LAWeights)
+    lib.gdn_la_block_workspace_size.argtypes = [LP, P, ctypes.c_int32, ctypes.POINTER(ctypes.c_size_t)]
+    lib.gdn_la_block_workspace_size.restype = ctypes.c_int
+    lib.gdn_la_block_replay.argtypes = [LP, WP, P, P, P, P, P, P, ctypes.c_size_t, P]
+    lib.gdn_la_block_replay.restype = ctypes.c_int
+    lib.gdn_la_block_replay_profiled.argtypes = lib.gdn_la_block_replay.argtypes + [P, ctypes.c_int32]
+    lib.gdn_la_block_replay_profiled.restype = ctypes.c_int
+    lib.gdn_la_block_num_stages.argtypes = [ctypes.c_int32]
+    lib.gdn_la_block_num_stages.restype = ctypes.c_int32
+    lib.gdn_la_block_stage_name.argtypes = [ctypes.c_int32, ctypes.c_int32]
+    lib.gdn_la_block_stage_name.restype = ctypes.c_char_p
     lib.gdn_replay_len.argtypes = [ctypes.c_int64, ctypes.c_int64, ctypes.c_int64]
     lib.gdn_replay_len.restype = ctypes.c_int64
     lib.gdn_status_string.argtypes = [ctypes.c_int]
@@ -447,3 +472,109 @@ def decode_step(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, g: torch.Tens
                                _ptr(state_in), _ptr(o), _ptr(state_out),
                                ctypes.c_void_p(stream.cuda_stream)))
     return o, state_out
+
+
+# ---------------------------------------------------------------- layer block
+
+LA_WEIGHT_NAMES = ("w_in", "conv_w", "a_log", "dt_bias", "norm_w", "w_out")
+
+
+def la_block_stage_names(with_outputs: bool):
+    """Names of the stages ``la_block_replay`` enqueues, in order."""
+    lib = load_library()
+    n = lib.gdn_la_block_num_stages(int(with_outputs))
+    return [lib.gdn_la_block_stage_name(int(with_outputs), i).decode() for i in range(n)]
+
+
+def _la_shape(n, hidden, hk, hv, dk, dv, act_dtype, scale, l2_eps, norm_eps):
+    code = {"f32": GDN_F32, "bf16": GDN_BF16}.get(act_dtype)
+    if code is None:
+        raise ValueError("act_dtype must be 'f32' or 'bf16'")
+    return LAShape(n, hidden, hk, hv, dk, dv, 4, code, float(scale), float(l2_eps), float(norm_eps))
+
+
+def la_block_workspace_size(hidden: int, num_k_heads: int, num_v_heads: int, d_k: int, d_v: int,
+                            cu_seqlens_host: Sequence[int], with_outputs: bool = True,
+                            act_dtype: str = "f32") -> int:
+    lib = load_library()
+    cu = torch.tensor(list(cu_seqlens_host), dtype=torch.int32)
+    shp = _la_shape(cu.numel() - 1, hidden, num_k_heads, num_v_heads, d_k, d_v, act_dtype, 1.0, 0.0, 0.0)
+    out = ctypes.c_size_t(0)
+    _check(lib.gdn_la_block_workspace_size(ctypes.byref(shp), _ptr(cu), int(with_outputs),
+                                           ctypes.byref(out)))
+    return int(out.value)
+
+
+def la_block_replay(x: torch.Tensor, weights, cu_seqlens, num_k_heads: int, num_v_heads: int,
+                    d_k: int, d_v: int, scale: float, cu_seqlens_host=None, outputs: bool = True,
+                    act_dtype: str = "f32", l2_eps: float = 1e-6, norm_eps: float = 1e-6,
+                    state_out: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                    workspace: Optional[torch.Tensor] = None, events=None):
+    """Replay of one linear-attention layer over packed tails (paper Section 3,
+    Eq. 2 behind the layer's projections) on torch's current stream.
+
+    x [T, D] bf16: the cached hiddens; ``weights``: mapping with w_in bf16
+    [2cq+2cv+2Hv, D] (rows q|k|v|a|b|z), conv_w fp32 [2cq+cv, 4], a_log and
+    dt_bias fp32 [Hv], norm_w fp32 [d_v], w_out bf16 [D, cv] (the last two
+    unused when ``outputs`` is False).  Returns ``(state_out [N,Hv,d_k,d_v]
+    fp32, out [T, D] bf16 or None)``.
+    """
+    lib = load_library()
+    device = x.device
+    _need(x, "x", torch.bfloat16, device, 2)
+    T, D = x.shape
+    cq, cv = num_k_heads * d_k, num_v_heads * d_v
+    specs = {"w_in": (torch.bfloat16, (2 * cq + 2 * cv + 2 * num_v_heads, D)),
+             "conv_w": (torch.float32, (2 * cq + cv, 4)),
+             "a_log": (torch.float32, (num_v_heads,)), "dt_bias": (torch.float32, (num_v_heads,)),
+             "norm_w": (torch.float32, (d_v,)), "w_out": (torch.bfloat16, (D, cv))}
+    ptrs = {}
+    for name in LA_WEIGHT_NAMES:
+        t = weights.get(name)
+        if t is None and not outputs and name in ("norm_w", "w_out"):
+            ptrs[name] = None
+            continue
+        dt, shp = specs[name]
+        _need(t, name, dt, device, len(shp))
+        if tuple(t.shape) != shp:
+            raise ValueError(f"{name} must be {list(shp)}, got {list(t.shape)}")
+        ptrs[name] = t.data_ptr()
+    w = LAWeights(*(ptrs[n] for n in LA_WEIGHT_NAMES))
+    cu_dev, cu_host = _seqlens(cu_seqlens, cu_seqlens_host, device)
+    n = cu_host.numel() - 1
+    if state_out is None:
+        state_out = torch.empty((n, num_v_heads, d_k, d_v), dtype=torch.float32, device=device)
+    _need(state_out, "state_out", torch.float32, device, 4)
+    if tuple(state_out.shape) != (n, num_v_heads, d_k, d_v):
+        raise ValueError("state_out must be [N, Hv, d_k, d_v]")
+    if outputs:
+        if out is None:
+            out = torch.empty((T, D), dtype=torch.bfloat16, device=device)
+        _need(out, "out", torch.bfloat16, device, 2)
+        if tuple(out.shape) != (T, D):
+            raise ValueError("out must be [T, D]")
+    else:
+        out = None
+    shp = _la_shape(n, D, num_k_heads, num_v_heads, d_k, d_v, act_dtype, scale, l2_eps, norm_eps)
+    stream = torch.cuda.current_stream(device)
+    need = ctypes.c_size_t(0)
+    _check(lib.gdn_la_block_workspace_size(ctypes.byref(shp), _ptr(cu_host), int(outputs),
+                                           ctypes.byref(need)))
+    ws = workspace if workspace is not None else _workspace(need.value, device, stream)
+    args = [ctypes.byref(shp), ctypes.byref(w), _ptr(cu_host), _ptr(cu_dev), _ptr(x), _ptr(state_out),
+            _ptr(out), _ptr(ws), ws.numel() * ws.element_size(), ctypes.c_void_p(stream.cuda_stream)]
+    if events is None:
+        _check(lib.gdn_la_block_replay(*args))
+    else:
+        ne = lib.gdn_la_block_num_stages(int(outputs)) + 1
+        if len(events) != ne:
+            raise ValueError(f"need {ne} events (one per stage boundary)")
+        handles = []
+        for ev in events:
+            if ev.cuda_event == 0:
+                ev.record()
+            handles.append(ev.cuda_event)
+        arr = (ctypes.c_void_p * ne)(*handles)
+        _check(lib.gdn_la_block_replay_profiled(*args, ctypes.cast(arr, ctypes.c_void_p), ne))
+    return state_out, out
+

@@ -15,7 +15,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_NAME = "libgdn_tailreplay.so"
 LIB_PATH = os.path.join(HERE, LIB_NAME)
-SOURCES = ["gdn_plan.cpp", "gdn_api.hip"]
+SOURCES = ["gdn_plan.cpp", "gdn_gemm.cpp", "gdn_api.hip", "gdn_block.hip"]
+ROCM_LIB = "/opt/rocm/lib"
 ARCH = "gfx950"
 
 
@@ -36,6 +37,8 @@ def build(verbose: bool = False) -> str:
            "-mllvm", "-amdgpu-mfma-vgpr-form",
            "-Wall", "-I", INCLUDE, "-I", CSRC, "-o", tmp]
     cmd += [os.path.join(CSRC, s) for s in SOURCES]
+    # the layer block's projections run through hipBLASLt
+    cmd += ["-L", ROCM_LIB, "-Wl,-rpath," + ROCM_LIB, "-lhipblaslt"]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)

@@ -31,8 +31,6 @@
 namespace gdn {
 namespace {
 
-thread_local std::string t_last_error;
-
 constexpr int kThreads = 256;
 // grid limits in make_plan assume <= 1024 work items per (sequence, head) in any
 // grid dimension; the column-split scan's grid is bounded by the CU count instead
@@ -40,7 +38,7 @@ static_assert(kThreads <= 256 && kDecodeThreads <= 1024 && head_threads(128) <= 
 
 // ------------------------------------------------------------ host side
 gdn_status fail(gdn_status st, const std::string& msg) {
-  t_last_error = msg;
+  set_last_error(msg);
   return st;
 }
 
@@ -575,6 +573,6 @@ const char* gdn_status_string(gdn_status status) {
   return "unknown gdn_status";
 }
 
-const char* gdn_last_error(void) { return gdn::t_last_error.c_str(); }
+const char* gdn_last_error(void) { return gdn::last_error(); }
 
 }  // extern "C"

@@ -16,6 +16,13 @@ constexpr int64_t kMaxGroups = std::numeric_limits<uint32_t>::max() / 256;
 
 }  // namespace
 
+namespace {
+thread_local std::string t_last_error;
+}  // namespace
+
+void set_last_error(const std::string& msg) { t_last_error = msg; }
+const char* last_error() { return t_last_error.c_str(); }
+
 gdn_status check_shape(const gdn_shape* shape, std::string* err) {
   if (!shape) { *err = "shape is NULL"; return GDN_ERR_NULL_ARG; }
   const int32_t N = shape->num_seqs, hk = shape->num_k_heads, hv = shape->num_v_heads;
@@ -92,6 +99,61 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   off = align_up(off + kSRecordBytes * recs);
   p.off_P = off;
   if (with_outputs) off = align_up(off + kPRecordBytes * recs);
+  p.bytes = off;
+  *plan = p;
+  return GDN_OK;
+}
+
+gdn_status make_block_plan(const gdn_la_shape* shape, const int32_t* cu, bool with_outputs,
+                           BlockPlan* plan, std::string* err) {
+  if (!plan) { *err = "plan is NULL"; return GDN_ERR_NULL_ARG; }
+  if (!shape) { *err = "shape is NULL"; return GDN_ERR_NULL_ARG; }
+  BlockPlan p;
+  p.scan = gdn_shape{shape->num_seqs, shape->num_k_heads, shape->num_v_heads, shape->d_k,
+                     shape->d_v, shape->act_dtype, shape->scale};
+  gdn_status st = make_plan(&p.scan, cu, with_outputs, &p.scan_plan, err);
+  if (st != GDN_OK) return st;
+  const int32_t hk = shape->num_k_heads, hv = shape->num_v_heads;
+  if (shape->hidden < 1) { *err = "hidden must be >= 1"; return GDN_ERR_BAD_SHAPE; }
+  if (shape->hidden % 8 != 0) { *err = "hidden must be a multiple of 8"; return GDN_ERR_UNSUPPORTED; }
+  if (shape->conv_taps != kBlockConvTaps) { *err = "conv_taps must be 4"; return GDN_ERR_UNSUPPORTED; }
+  if (hv % 4 != 0) { *err = "num_v_heads must be a multiple of 4"; return GDN_ERR_UNSUPPORTED; }
+  if (!std::isfinite(shape->l2_eps) || !std::isfinite(shape->norm_eps) || shape->l2_eps < 0.0f ||
+      shape->norm_eps < 0.0f) {
+    *err = "l2_eps and norm_eps must be finite and >= 0";
+    return GDN_ERR_BAD_SHAPE;
+  }
+  p.T = p.scan_plan.total_tokens;
+  p.outputs = with_outputs;
+  p.cq = static_cast<int64_t>(hk) * shape->d_k;
+  p.cv = static_cast<int64_t>(hv) * shape->d_v;
+  const int64_t all_rows = 2 * p.cq + 2 * p.cv + 2 * hv;
+  p.row0 = with_outputs ? 0 : p.cq;
+  p.rows = with_outputs ? all_rows : p.cq + p.cv + 2 * hv;   // k | v | a | b
+  p.ldp = p.rows;                                            // a multiple of 8 (Hv % 4 == 0)
+  p.act_bytes = shape->act_dtype == GDN_F32 ? 4 : 2;
+  const int64_t nch = with_outputs ? 2 * p.cq + p.cv : p.cq + p.cv;   // channels the prep computes
+  p.prep_token_blocks = (p.T + 15) / 16;
+  p.prep_slabs = (nch + 2047) / 2048 + 1;
+  p.norm_blocks = with_outputs ? (p.T * p.cv / 8 + 255) / 256 : 0;
+  if (p.T > std::numeric_limits<int32_t>::max() / 2 ||
+      p.prep_token_blocks * p.prep_slabs > std::numeric_limits<int32_t>::max() ||
+      p.norm_blocks > std::numeric_limits<int32_t>::max()) {
+    *err = "too many tokens for one call";
+    return GDN_ERR_UNSUPPORTED;
+  }
+  const size_t T = static_cast<size_t>(p.T), es = p.act_bytes;
+  size_t off = 0;
+  auto take = [&](size_t bytes) { const size_t at = off; off = align_up(off + bytes); return at; };
+  p.off_P = take(T * p.ldp * es);
+  p.off_q = with_outputs ? take(T * p.cq * es) : 0;
+  p.off_k = take(T * p.cq * es);
+  p.off_v = take(T * p.cv * es);
+  p.off_g = take(T * hv * 4);
+  p.off_beta = take(T * hv * 4);
+  p.off_o = with_outputs ? take(T * p.cv * es) : 0;
+  p.off_scan = take(p.scan_plan.bytes);
+  p.off_gemm = take(kGemmWorkspace);
   p.bytes = off;
   *plan = p;
   return GDN_OK;

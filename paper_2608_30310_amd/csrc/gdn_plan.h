@@ -6,6 +6,7 @@
 #include <cstdint>
 #include <string>
 
+#include "gdn_la_block.h"
 #include "gdn_tail_replay.h"
 
 namespace gdn {
@@ -55,6 +56,37 @@ struct Plan {
   size_t off_P = 0;               // [num_slots, Hv] P fragments (outputs only)
   size_t bytes = 0;               // total workspace size
 };
+
+// ---------------------------------------------------------------- layer block
+// Workspace the two projections may use (hipBLASLt's split-k kernels).
+constexpr size_t kGemmWorkspace = size_t{32} << 20;
+constexpr int kBlockConvTaps = 4;
+
+// Regions of the layer block's workspace and the in-projection's extent.  P
+// holds rows row0 .. row0 + rows of W_in applied to every token, pitch ldp.
+// With outputs, y (bf16 [T, cv]) reuses the q | k | v region once the
+// recurrence has consumed it.
+struct BlockPlan {
+  gdn_shape scan{};       // the recurrence's shape (qkv_dtype = act_dtype)
+  Plan scan_plan;         // and its workspace plan
+  int64_t T = 0;
+  bool outputs = false;
+  int64_t cq = 0, cv = 0;
+  int64_t row0 = 0, rows = 0, ldp = 0;
+  size_t act_bytes = 0;
+  size_t off_P = 0, off_q = 0, off_k = 0, off_v = 0, off_g = 0, off_beta = 0, off_o = 0;
+  size_t off_scan = 0, off_gemm = 0, bytes = 0;
+  int64_t prep_token_blocks = 0, prep_slabs = 0;   // channel slabs, plus one gate slab
+  int64_t norm_blocks = 0;
+};
+
+// Validates a layer-block call's shape and offsets and fills `plan`.
+gdn_status make_block_plan(const gdn_la_shape* shape, const int32_t* cu_seqlens_host,
+                           bool with_outputs, BlockPlan* plan, std::string* err);
+
+// The thread-local message behind gdn_last_error(), shared by every entry point.
+void set_last_error(const std::string& msg);
+const char* last_error();
 
 // Validates the shape alone (dimensions, dtype, scale, grid limits).
 gdn_status check_shape(const gdn_shape* shape, std::string* err);

@@ -6,6 +6,7 @@ pointers are placeholders that are never dereferenced; on a machine with a GPU
 these cases are skipped so no placeholder can ever reach a kernel.
 """
 import ctypes
+import glob
 import os
 import re
 
@@ -17,13 +18,13 @@ import paper_2608_30310_amd as gdn
 from paper_2608_30310_amd import binding
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "gdn_tail_replay.h")
+HEADERS = sorted(glob.glob(os.path.join(ROOT, "include", "*.h")))
 
 FAKE = ctypes.c_void_p(0x1000)   # never dereferenced: validation fails first
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(gdn_[a-z_]+)\s*\(", text)))
 
@@ -32,7 +33,8 @@ def test_header_declares_the_boundary():
     names = declared_functions()
     for want in ("gdn_tail_replay", "gdn_chunk_forward", "gdn_workspace_size",
                  "gdn_replay_forward", "gdn_replay_forward_workspace_size",
-                 "gdn_replay_len", "gdn_status_string", "gdn_last_error"):
+                 "gdn_replay_len", "gdn_status_string", "gdn_last_error", "gdn_decode_step",
+                 "gdn_la_block_replay", "gdn_la_block_workspace_size"):
         assert want in names
 
 
