@@ -75,11 +75,11 @@ def parse():
                     help="with --summarize-pmc: workload description stored in the summary")
     ap.add_argument("--sweep", action="store_true",
                     help="time the other workloads instead (one JSON line each): small fp32 layer, "
-                         "36-layer stack, 16 varlen hits, decode steps, FA-KV transfer overlap, "
+                         "36-layer stack, 16 varlen hits, decode steps, FA-KV transfer overlap, layer-block replay, "
                          "replay-vs-full at 8K/16K/32K")
     ap.add_argument("--only", default="",
                     help="with --sweep: comma list of sections to run "
-                         "(small, layer410, stack, hits, decode, h2d, full)")
+                         "(small, layer410, stack, hits, decode, h2d, block, full)")
     ap.add_argument("--decode-seqs", default="1,64,256",
                     help="with --sweep: batch sizes of the decode lines")
     return ap.parse_args()
@@ -713,6 +713,71 @@ def sweep(args):
                   "ovl_vs_ser_reduction": 1 - t_ovl["p50"] / t_ser["p50"],
                   "hidden_fraction_of_shorter": hidden})
             del host_kv, dev_kv, xl, xq
+
+    # ---- the whole linear-attention layer replayed from the cached hiddens
+    #      (in-projection, conv, norms, gates, recurrence, gated norm,
+    #      out-projection) at D = 2048, Hk = 16, Hv = 32, d = 128; weights and
+    #      hiddens drawn on the device with the layer recipe's ranges (timing
+    #      only).  "outputs": a layer whose output feeds the next layer of the
+    #      group; "state only": the group's last layer (no q, z or output path,
+    #      no feed-forward block).  Per-stage times from the library's stage
+    #      events; the projections are priced against the bf16 MFMA peak.
+    if want("block"):
+        D, hk, hv, d = 2048, 16, 32, 128
+        cq, cv = hk * d, hv * d
+        gen = torch.Generator(device=dev).manual_seed(77)
+
+        def dev_weights():
+            rn = lambda *s: torch.randn(*s, device=dev, generator=gen)
+            return dict(w_in=(rn(2 * cq + 2 * cv + 2 * hv, D) / D ** 0.5).to(torch.bfloat16),
+                        conv_w=(torch.rand(2 * cq + cv, 4, device=dev, generator=gen) - 0.5),
+                        a_log=torch.log(1 + 15 * torch.rand(hv, device=dev, generator=gen)),
+                        dt_bias=torch.full((hv,), -4.0, device=dev),
+                        norm_w=0.5 + torch.rand(d, device=dev, generator=gen),
+                        w_out=(rn(D, cv) / cv ** 0.5).to(torch.bfloat16))
+
+        wts = dev_weights()
+
+        def block_line(lens, outputs, act, label):
+            T = int(sum(lens))
+            cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+            cu_d, cu_h = torch.from_numpy(cu).to(dev), torch.from_numpy(cu)
+            x = torch.randn(T, D, device=dev, generator=gen).to(torch.bfloat16)
+            st = torch.empty((len(lens), hv, d, d), dtype=torch.float32, device=dev)
+            out = torch.empty((T, D), dtype=torch.bfloat16, device=dev) if outputs else None
+            ws = torch.empty(gdn.la_block_workspace_size(D, hk, hv, d, d, cu.tolist(), outputs, act) + 256,
+                             dtype=torch.uint8, device=dev)
+            call = lambda ev=None: gdn.la_block_replay(x, wts, cu_d, hk, hv, d, d, d ** -0.5, cu_seqlens_host=cu_h,
+                                                       outputs=outputs, act_dtype=act, state_out=st, out=out,
+                                                       workspace=ws, events=ev)
+            t = timed_us(call)
+            names = gdn.la_block_stage_names(outputs)
+            per = {n: [] for n in names}
+            for _ in range(reps):
+                ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(names) + 1)]
+                call(ev)
+                torch.cuda.synchronize()
+                for i, n in enumerate(names):
+                    per[n].append(ev[i].elapsed_time(ev[i + 1]) * 1e3)
+            stages = {n: float(np.median(v)) for n, v in per.items()}
+            rows = 2 * cq + 2 * cv + 2 * hv if outputs else cq + cv + 2 * hv
+            fl_in = 2.0 * T * D * rows
+            rec = {"workload": f"LA layer replay D={D} Hk={hk} Hv={hv} d={d}, {label}, "
+                               f"{'outputs' if outputs else 'state only'}, {act} intermediates",
+                   "tokens": T, "us": t["p50"], "tokens_per_s": T / (t["p50"] * 1e-6),
+                   "stage_us": stages,
+                   "in_proj_tflops": fl_in / (stages["in-projection"] * 1e-6) / 1e12,
+                   "in_proj_frac_of_bf16_peak": fl_in / (stages["in-projection"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS}
+            if outputs:
+                fl_out = 2.0 * T * cv * D
+                rec["out_proj_tflops"] = fl_out / (stages["out-projection"] * 1e-6) / 1e12
+            emit(rec)
+            return t["p50"]
+
+        for act in ("f32", "bf16"):
+            for lens, label in (([819], "tail 819 (10% of 8192)"), ([3277], "tail 3277 (10% of 32768)")):
+                block_line(lens, True, act, label)
+                block_line(lens, False, act, label)
 
     # ---- replay vs full prefill, suffix 512: t_full = forward(0, m + s) with
     #      outputs; t_replay = the fused replay(r) + forward(S_m, s); state-only

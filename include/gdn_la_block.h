@@ -46,7 +46,7 @@
  * hipBLASLt; their workspace is part of the caller's), and `out` may alias
  * `x` (x is read only by the in-projection, before out is written).
  * Requirements: D % 8 == 0, Hv % 4 == 0, d_k and d_v in {64, 128}, Hv % Hk == 0,
- * conv_taps == 4; x, w_in, w_out, out and conv_w 16-byte aligned; workspace
+ * conv_taps == 4; x, w_in, w_out, out, conv_w and norm_w 16-byte aligned; workspace
  * 256-byte aligned.
  */
 #ifndef GDN_LA_BLOCK_H

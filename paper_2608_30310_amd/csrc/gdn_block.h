@@ -20,16 +20,21 @@
 namespace gdn {
 
 constexpr int kPrepThreads = 256;
-constexpr int kPrepTokens = 16;   // tokens per workgroup: the conv window slides in registers
+constexpr int kPrepChans = 256;   // channels per prep workgroup (32 threads x 8)
+constexpr int kPrepTokens = kPrepThreads / (kPrepChans / 8);   // 8 tokens per workgroup
 constexpr int kConvTaps = 4;
 constexpr int kNormThreads = 256;
 
 template <typename T>
 __device__ __forceinline__ void store8(T* __restrict__ p, const float (&x)[8]) {
   if constexpr (sizeof(T) == 2) {
+    // the hardware pair conversion rounds to nearest even, as f2bf does
     u32x4 w;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) w[j] = f2bf(x[2 * j]) | (static_cast<uint32_t>(f2bf(x[2 * j + 1])) << 16);
+    for (int j = 0; j < 4; ++j) {
+      const f32x2 pair = {x[2 * j], x[2 * j + 1]};
+      w[j] = __builtin_bit_cast(uint32_t, __builtin_convertvector(pair, bf16x2));
+    }
     *reinterpret_cast<u32x4*>(p) = w;
   } else {
     reinterpret_cast<f32x4*>(p)[0] = f32x4{x[0], x[1], x[2], x[3]};
@@ -37,7 +42,9 @@ __device__ __forceinline__ void store8(T* __restrict__ p, const float (&x)[8]) {
   }
 }
 
-__device__ __forceinline__ float silu_f(float x) { return x / (1.0f + expf(-x)); }
+// x sigmoid(x) with the hardware exponential and reciprocal (about 1e-7
+// relative; x far below zero gives exp = inf, rcp = 0 and -0)
+__device__ __forceinline__ float silu_f(float x) { return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
 
 // Sequence of token t (0 <= t < cu[n_seqs]): the largest n with cu[n] <= t,
 // which skips empty sequences.
@@ -50,29 +57,25 @@ __device__ __forceinline__ int seq_of(const int32_t* __restrict__ cu, int n_seqs
   return lo;
 }
 
-// P [T, ldp] (TP) holds the in-projection from channel chan0 on: q|k|v
-// channels chan0 .. 2 cq + cv, then a [hv], then b [hv].  chan0 = 0 computes
-// q, k and v; chan0 = cq (no queries) k and v only.  Grid: xcd-remapped
-// 1-D, logical index = slab * token_blocks + token_block, slabs = chan_slabs
-// channel slabs of 2048 channels plus one gate slab.
+// One unit of k_la_prep: channel slab `slab` (or the gates when slab ==
+// chan_slabs) of token block `tb`.
 template <typename TP, typename TQ, int DK, int DV>
-__global__ __launch_bounds__(kPrepThreads)
-void k_la_prep(int32_t T, int32_t n_seqs, const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
-               const TP* __restrict__ P, int64_t ldp, int32_t chan0, int32_t chan_slabs,
-               int32_t token_blocks, const float* __restrict__ conv_w, const float* __restrict__ a_log,
-               const float* __restrict__ dt_bias, float l2_eps, TQ* __restrict__ q,
-               TQ* __restrict__ k, TQ* __restrict__ v, float* __restrict__ g,
-               float* __restrict__ beta) {
-  const int total = token_blocks * (chan_slabs + 1);
-  const int logical = xcd_remap(blockIdx.x, total);
-  const int slab = logical / token_blocks, tb = logical % token_blocks;
+__device__ __forceinline__ void prep_unit(int slab, int tb, int32_t T, int32_t n_seqs,
+                                          const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
+                                          const TP* __restrict__ P, int64_t ldp, int32_t chan0,
+                                          int32_t chan_slabs, const float* __restrict__ conv_w,
+                                          const float* __restrict__ a_log, const float* __restrict__ dt_bias,
+                                          float l2_eps, TQ* __restrict__ q, TQ* __restrict__ k,
+                                          TQ* __restrict__ v, float* __restrict__ g, float* __restrict__ beta,
+                                          float (*wlds)[kPrepChans]) {
+  constexpr int H = kConvTaps - 1;
   const int cq = hk * DK, cv = hv * DV, nch = 2 * cq + cv;
   const int t0 = tb * kPrepTokens;
-  const int t1 = min(T, t0 + kPrepTokens);
   const int tid = threadIdx.x;
 
   if (slab == chan_slabs) {   // gates
     const int ca = nch - chan0;
+    const int t1 = min(T, t0 + kPrepTokens);
     for (int i = tid; i < (t1 - t0) * hv; i += kPrepThreads) {
       const int t = t0 + i / hv, h = i % hv;
       const TP* row = P + static_cast<int64_t>(t) * ldp;
@@ -85,77 +88,120 @@ void k_la_prep(int32_t T, int32_t n_seqs, const int32_t* __restrict__ cu, int32_
     return;
   }
 
-  const int c0 = chan0 + (slab * kPrepThreads + tid) * 8;
-  const bool active = c0 < nch;      // idle lanes still join the lane exchanges
-  const int sec = c0 < cq ? 0 : (c0 < 2 * cq ? 1 : 2);
-  TQ* dst;
-  int64_t ld;
-  if (sec == 0) { dst = q + c0; ld = cq; }
-  else if (sec == 1) { dst = k + (c0 - cq); ld = cq; }
-  else { dst = v + (c0 - 2 * cq); ld = cv; }
-  float w[8][kConvTaps];
+  const int t = t0 + tid / (kPrepChans / 8);
+  const int cg = tid % (kPrepChans / 8);
+  const int c0 = chan0 + (slab * (kPrepChans / 8) + cg) * 8;
+  const bool active = c0 < nch && t < T;   // idle lanes still join the lane exchanges
+  // Every global load of the unit is issued before anything waits: the
+  // slab's conv taps (one coalesced 16-byte load per thread, channel
+  // slab * 256 + tid), the first token of this token's sequence, and the four
+  // rows t - 3 .. t (those before the sequence are zeroed afterwards).
+  const int ch = chan0 + slab * kPrepChans + tid;
+  const float4 w4 = ch < nch ? reinterpret_cast<const float4*>(conv_w)[ch] : make_float4(0.f, 0.f, 0.f, 0.f);
+  int first = 0;
+  float u[kConvTaps][8];
+  if (active) {
+    first = cu[seq_of(cu, n_seqs, t)];
+    const TP* col = P + (c0 - chan0);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const float4 t4 = active ? reinterpret_cast<const float4*>(conv_w)[c0 + i] : make_float4(0.f, 0.f, 0.f, 0.f);
-    w[i][0] = t4.x; w[i][1] = t4.y; w[i][2] = t4.z; w[i][3] = t4.w;
+    for (int j = 0; j < kConvTaps; ++j) {
+      const int tj = t - H + j;
+      if (tj >= 0) {
+        load_run<TP, 8>(col + static_cast<int64_t>(tj) * ldp, u[j]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) u[j][e] = 0.0f;
+      }
+    }
   }
-  const TP* col = P + (c0 - chan0);
+  // the taps, tap-major in LDS; each thread then reads its eight channels of
+  // each tap as two 16-byte LDS reads
+  lds_barrier();   // the previous unit's LDS readers are done
+  wlds[0][tid] = w4.x;
+  wlds[1][tid] = w4.y;
+  wlds[2][tid] = w4.z;
+  wlds[3][tid] = w4.w;
+  lds_barrier();
+  float c[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) c[e] = 0.0f;
+  if (active) {
+    float w[kConvTaps][8];
+#pragma unroll
+    for (int j = 0; j < kConvTaps; ++j) {
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(&wlds[j][cg * 8]);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(&wlds[j][cg * 8 + 4]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) { w[j][e] = lo[e]; w[j][4 + e] = hi[e]; }
+      if (t - H + j < first) {   // before the sequence: zero history
+#pragma unroll
+        for (int e = 0; e < 8; ++e) u[j][e] = 0.0f;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      c[e] = silu_f(w[0][e] * u[0][e] + w[1][e] * u[1][e] + w[2][e] * u[2][e] + w[3][e] * u[3][e]);
+  }
+  float ss = 0.0f;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) ss += c[e] * c[e];
+  // sum of squares over the head (DK / 8 lanes); used by q and k lanes only
+#pragma unroll
+  for (int off = 1; off < DK / 8; off <<= 1) ss += __shfl_xor(ss, off, kWave);
+  if (!active) return;
+  const int sec = c0 < cq ? 0 : (c0 < 2 * cq ? 1 : 2);
+  if (sec < 2) {
+    const float r = rsqrtf(ss + l2_eps);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) c[e] *= r;
+  }
+  TQ* dst;
+  if (sec == 0) dst = q + static_cast<int64_t>(t) * cq + c0;
+  else if (sec == 1) dst = k + static_cast<int64_t>(t) * cq + (c0 - cq);
+  else dst = v + static_cast<int64_t>(t) * cv + (c0 - 2 * cq);
+  store8(dst, c);
+}
 
-  int n = seq_of(cu, n_seqs, t0);
-  int start = cu[n];
-  int next = cu[n + 1];
-  float u1[8], u2[8], u3[8];   // u[t-1], u[t-2], u[t-3]
-  auto row = [&](int t, float (&x)[8]) {
-    if (active && t >= start) {
-      load_run<TP, 8>(col + static_cast<int64_t>(t) * ldp, x);
-    } else {
-#pragma unroll
-      for (int i = 0; i < 8; ++i) x[i] = 0.0f;
-    }
-  };
-  row(t0 - 1, u1);
-  row(t0 - 2, u2);
-  row(t0 - 3, u3);
-  for (int t = t0; t < t1; ++t) {
-    if (t == next) {   // a sequence starts here: its convolution history is zero
-      while (cu[n + 1] <= t) ++n;
-      start = t;
-      next = cu[n + 1];
-#pragma unroll
-      for (int i = 0; i < 8; ++i) u1[i] = u2[i] = u3[i] = 0.0f;
-    }
-    float u0[8];
-    row(t, u0);
-    float c[8], ss = 0.0f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const float s = w[i][0] * u3[i] + w[i][1] * u2[i] + w[i][2] * u1[i] + w[i][3] * u0[i];
-      c[i] = silu_f(s);
-      ss += c[i] * c[i];
-    }
-    // sum of squares over the head (DK / 8 lanes); used by q and k lanes only
-#pragma unroll
-    for (int off = 1; off < DK / 8; off <<= 1) ss += __shfl_xor(ss, off, kWave);
-    if (sec < 2) {
-      const float r = rsqrtf(ss + l2_eps);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) c[i] *= r;
-    }
-    if (active) store8(dst + static_cast<int64_t>(t) * ld, c);
-#pragma unroll
-    for (int i = 0; i < 8; ++i) { u3[i] = u2[i]; u2[i] = u1[i]; u1[i] = u0[i]; }
+// P [T, ldp] (TP) holds the in-projection from channel chan0 on: q|k|v
+// channels chan0 .. 2 cq + cv, then a [hv], then b [hv].  chan0 = 0 computes
+// q, k and v; chan0 = cq (no queries) k and v only.
+// One thread per (token, eight channels): a workgroup covers kPrepTokens
+// tokens x kPrepChans channels, thread (tok, cg) = (tid / 32, tid % 32), and
+// loads the four rows its taps need (the neighbours' rows come from L1).
+// Units: chan_slabs channel slabs plus one gate slab per token block; unit u
+// is xcd-remapped to logical index token_block * (chan_slabs + 1) + slab, so
+// an XCD streams whole rows of P, token after token.  The
+// grid is sized to the machine (a few workgroups per CU) and strides over the
+// units, so waves live long enough to keep many loads in flight: one short
+// wave per unit leaves the CUs mostly waiting for wave launches.  The stride
+// is a multiple of 8, so a unit runs on the XCD its remap assumes.
+template <typename TP, typename TQ, int DK, int DV>
+__global__ __launch_bounds__(kPrepThreads)
+void k_la_prep(int32_t T, int32_t n_seqs, const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
+               const TP* __restrict__ P, int64_t ldp, int32_t chan0, int32_t chan_slabs,
+               int32_t token_blocks, const float* __restrict__ conv_w, const float* __restrict__ a_log,
+               const float* __restrict__ dt_bias, float l2_eps, TQ* __restrict__ q,
+               TQ* __restrict__ k, TQ* __restrict__ v, float* __restrict__ g,
+               float* __restrict__ beta) {
+  __shared__ __attribute__((aligned(16))) float wlds[kConvTaps][kPrepChans];
+  const int total = token_blocks * (chan_slabs + 1);
+  for (int unit = blockIdx.x; unit < total; unit += gridDim.x) {   // uniform per workgroup
+    const int logical = xcd_remap(unit, total);
+    const int slabs = chan_slabs + 1;
+    prep_unit<TP, TQ, DK, DV>(logical % slabs, logical / slabs, T, n_seqs, cu, hk, hv, P,
+                              ldp, chan0, chan_slabs, conv_w, a_log, dt_bias, l2_eps, q, k, v, g, beta,
+                              wlds);
   }
 }
 
-// o [T, hv, DV] (TO); z at P[t, col_z + h DV + j] (TP); y [T, hv DV] bf16.
-// One thread per eight channels, groups = T hv DV / 8.
+
+// One group of k_gated_norm: the eight channels from element e = 8 i of
+// y [T, hv DV]; `active` false for the padding lanes past the end, which only
+// join the lane exchange.
 template <typename TO, typename TP, int DV>
-__global__ __launch_bounds__(kNormThreads)
-void k_gated_norm(int64_t groups, int32_t cv, const TO* __restrict__ o, const TP* __restrict__ P,
-                  int64_t ldp, int32_t col_z, const float* __restrict__ w_norm, float eps,
-                  uint16_t* __restrict__ y) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * kNormThreads + threadIdx.x;
-  const bool active = i < groups;    // whole heads are active or idle together
+__device__ __forceinline__ void norm_group(int64_t i, bool active, int32_t cv, const TO* __restrict__ o,
+                                           const TP* __restrict__ P, int64_t ldp, int32_t col_z,
+                                           const float* __restrict__ w_norm, float eps, uint16_t* __restrict__ y) {
   const int64_t e = i * 8;
   const int64_t t = e / cv;
   const int c = static_cast<int>(e - t * cv);
@@ -175,10 +221,31 @@ void k_gated_norm(int64_t groups, int32_t cv, const TO* __restrict__ o, const TP
   const float r = rsqrtf(ss * (1.0f / DV) + eps);
   if (!active) return;
   const int cj = c % DV;
+  const f32x4 w0 = *reinterpret_cast<const f32x4*>(w_norm + cj);
+  const f32x4 w1 = *reinterpret_cast<const f32x4*>(w_norm + cj + 4);
   float out[8];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) out[j] = ov[j] * r * w_norm[cj + j] * silu_f(zv[j]);
+  for (int j = 0; j < 4; ++j) {
+    out[j] = ov[j] * r * w0[j] * silu_f(zv[j]);
+    out[4 + j] = ov[4 + j] * r * w1[j] * silu_f(zv[4 + j]);
+  }
   store8(y + e, out);
+}
+
+// o [T, hv, DV] (TO); z at P[t, col_z + h DV + j] (TP); y [T, hv DV] bf16.
+// One thread per eight channels, groups = T hv DV / 8, a whole head (DV / 8
+// lanes) active or idle together; the grid strides over the groups (sized to
+// the machine, as for k_la_prep).
+template <typename TO, typename TP, int DV>
+__global__ __launch_bounds__(kNormThreads)
+void k_gated_norm(int64_t groups, int32_t cv, const TO* __restrict__ o, const TP* __restrict__ P,
+                  int64_t ldp, int32_t col_z, const float* __restrict__ w_norm, float eps,
+                  uint16_t* __restrict__ y) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kNormThreads;
+  for (int64_t base = static_cast<int64_t>(blockIdx.x) * kNormThreads; base < groups; base += stride) {
+    const int64_t i = base + threadIdx.x;
+    norm_group<TO, TP, DV>(i, i < groups, cv, o, P, ldp, col_z, w_norm, eps, y);
+  }
 }
 
 }  // namespace gdn

@@ -23,6 +23,9 @@
 namespace gdn {
 namespace {
 
+static_assert(kPrepTokens == kBlockPrepTokens && kPrepChans == kBlockPrepChans && kConvTaps == kBlockConvTaps,
+              "host and device tiling agree");
+
 constexpr int32_t kBlockStagesOut = 5;
 constexpr int32_t kBlockStagesState = 3;
 const char* const kBlockStageNamesOut[kBlockStagesOut] = {"in-projection", "prep", "recurrence",
@@ -48,7 +51,7 @@ struct Marks {
 template <typename TA, int DK, int DV>
 void launch_prep(const BlockPlan& p, const gdn_la_shape& s, const gdn_la_weights& w, const int32_t* cu,
                  char* ws, hipStream_t stream) {
-  const uint32_t blocks = static_cast<uint32_t>(p.prep_token_blocks * p.prep_slabs);
+  const uint32_t blocks = static_cast<uint32_t>(p.prep_grid);
   TA* q = p.outputs ? reinterpret_cast<TA*>(ws + p.off_q) : nullptr;
   hipLaunchKernelGGL((k_la_prep<TA, TA, DK, DV>), dim3(blocks), dim3(kPrepThreads), 0, stream,
                      static_cast<int32_t>(p.T), s.num_seqs, cu, s.num_k_heads, s.num_v_heads,
@@ -64,7 +67,7 @@ void launch_norm(const BlockPlan& p, const gdn_la_shape& s, const gdn_la_weights
                  hipStream_t stream) {
   const int64_t groups = p.T * p.cv / 8;
   const int32_t col_z = static_cast<int32_t>(2 * p.cq + p.cv + 2 * s.num_v_heads);
-  hipLaunchKernelGGL((k_gated_norm<TA, TA, DV>), dim3(static_cast<uint32_t>(p.norm_blocks)),
+  hipLaunchKernelGGL((k_gated_norm<TA, TA, DV>), dim3(static_cast<uint32_t>(p.norm_grid)),
                      dim3(kNormThreads), 0, stream, groups, static_cast<int32_t>(p.cv),
                      reinterpret_cast<const TA*>(ws + p.off_o), reinterpret_cast<const TA*>(ws + p.off_P),
                      p.ldp, col_z, w.norm_w, s.norm_eps, reinterpret_cast<uint16_t*>(ws + p.off_q));
@@ -120,8 +123,8 @@ gdn_status block_impl(const gdn_la_shape* shape, const gdn_la_weights* w, const 
   if (shape->num_seqs > 0 && !cu) return bfail(GDN_ERR_NULL_ARG, "cu_seqlens (device) is NULL");
   if (p.T > 0 && !x) return bfail(GDN_ERR_NULL_ARG, "x is NULL");
   if (misaligned(x, 16) || misaligned(w->w_in, 16) || misaligned(w->conv_w, 16) ||
-      (outputs && (misaligned(w->w_out, 16) || misaligned(out, 16))))
-    return bfail(GDN_ERR_UNSUPPORTED, "x, w_in, conv_w, w_out and out must be 16-byte aligned");
+      (outputs && (misaligned(w->w_out, 16) || misaligned(w->norm_w, 16) || misaligned(out, 16))))
+    return bfail(GDN_ERR_UNSUPPORTED, "x, w_in, conv_w, norm_w, w_out and out must be 16-byte aligned");
   if (!workspace) return bfail(GDN_ERR_WORKSPACE, "workspace is NULL");
   if (workspace_bytes < p.bytes)
     return bfail(GDN_ERR_WORKSPACE, "workspace too small: need " + std::to_string(p.bytes) + " bytes, got " +

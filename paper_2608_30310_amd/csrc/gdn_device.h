@@ -29,6 +29,12 @@ __device__ __forceinline__ int xcd_remap(int b, int total) {
   return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
 }
 
+// Barrier for data exchanged through LDS: waits for this wave's LDS accesses
+// only (not for its outstanding global loads, DMA or stores, as
+// __syncthreads does), and keeps the compiler from moving memory accesses
+// across it.
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // ---------------------------------------------------------------- bf16
 __device__ __forceinline__ uint16_t f2bf(float x) {
   // round to nearest, ties to even (finite values)

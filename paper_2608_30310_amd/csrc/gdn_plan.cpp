@@ -133,9 +133,11 @@ gdn_status make_block_plan(const gdn_la_shape* shape, const int32_t* cu, bool wi
   p.ldp = p.rows;                                            // a multiple of 8 (Hv % 4 == 0)
   p.act_bytes = shape->act_dtype == GDN_F32 ? 4 : 2;
   const int64_t nch = with_outputs ? 2 * p.cq + p.cv : p.cq + p.cv;   // channels the prep computes
-  p.prep_token_blocks = (p.T + 15) / 16;
-  p.prep_slabs = (nch + 2047) / 2048 + 1;
+  p.prep_token_blocks = (p.T + kBlockPrepTokens - 1) / kBlockPrepTokens;
+  p.prep_slabs = (nch + kBlockPrepChans - 1) / kBlockPrepChans + 1;
   p.norm_blocks = with_outputs ? (p.T * p.cv / 8 + 255) / 256 : 0;
+  p.prep_grid = std::min(p.prep_token_blocks * p.prep_slabs, kBlockElementwiseGroups);
+  p.norm_grid = std::min(p.norm_blocks, kBlockElementwiseGroups);
   if (p.T > std::numeric_limits<int32_t>::max() / 2 ||
       p.prep_token_blocks * p.prep_slabs > std::numeric_limits<int32_t>::max() ||
       p.norm_blocks > std::numeric_limits<int32_t>::max()) {

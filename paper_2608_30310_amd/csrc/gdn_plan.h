@@ -61,6 +61,11 @@ struct Plan {
 // Workspace the two projections may use (hipBLASLt's split-k kernels).
 constexpr size_t kGemmWorkspace = size_t{32} << 20;
 constexpr int kBlockConvTaps = 4;
+constexpr int kBlockPrepTokens = 8;   // tokens per prep workgroup (kPrepTokens on the device)
+constexpr int kBlockPrepChans = 256;  // channels per prep workgroup (kPrepChans)
+// Grid cap of the two elementwise kernels: 8 workgroups of 256 threads per CU
+// of the 256-CU MI355X (a multiple of 8, one per XCD); they stride over the rest.
+constexpr int64_t kBlockElementwiseGroups = 2048;
 
 // Regions of the layer block's workspace and the in-projection's extent.  P
 // holds rows row0 .. row0 + rows of W_in applied to every token, pitch ldp.
@@ -77,7 +82,8 @@ struct BlockPlan {
   size_t off_P = 0, off_q = 0, off_k = 0, off_v = 0, off_g = 0, off_beta = 0, off_o = 0;
   size_t off_scan = 0, off_gemm = 0, bytes = 0;
   int64_t prep_token_blocks = 0, prep_slabs = 0;   // channel slabs, plus one gate slab
-  int64_t norm_blocks = 0;
+  int64_t prep_grid = 0;                            // workgroups launched (<= units)
+  int64_t norm_blocks = 0, norm_grid = 0;
 };
 
 // Validates a layer-block call's shape and offsets and fills `plan`.

@@ -43,11 +43,6 @@ __device__ __forceinline__ void dma16(const void* src, lds_byte* dst) {
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// Barrier for data exchanged through LDS: waits for this wave's LDS accesses
-// only (not for its outstanding global loads, DMA or stores, as
-// __syncthreads does), and keeps the compiler from moving memory accesses
-// across it.
-__device__ __forceinline__ void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
 
 // Byte offset of byte `byte_in_row` of row `row` in a row tile whose rows hold
 // ROW_BYTES / 16 pieces of 16 bytes, piece p of row R stored at p ^ (R % pieces).

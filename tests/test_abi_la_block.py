@@ -85,7 +85,7 @@ needs_no_gpu = pytest.mark.skipif(torch.cuda.is_available(),
                                   reason="placeholder pointers are only used without a GPU")
 
 CASES = {"null_weights": 1, "null_w_in": 1, "null_w_out": 1, "null_state": 1, "null_x": 1, "null_cu": 1,
-         "misaligned_x": 4, "misaligned_conv_w": 4, "misaligned_out": 4, "small_ws": 5, "null_ws": 5,
+         "misaligned_x": 4, "misaligned_conv_w": 4, "misaligned_norm_w": 4, "misaligned_out": 4, "small_ws": 5, "null_ws": 5,
          "misaligned_ws": 5, "bad_hidden": 4, "bad_events": 2}
 
 
@@ -103,6 +103,8 @@ def test_block_rejects_before_launch(case):
         w.w_out = None
     if case == "misaligned_conv_w":
         w.conv_w = 0x1004
+    if case == "misaligned_norm_w":
+        w.norm_w = 0x1008
     x = None if case == "null_x" else (ctypes.c_void_p(0x1008) if case == "misaligned_x" else FAKE)
     out = ctypes.c_void_p(0x1002) if case == "misaligned_out" else FAKE
     ws = None if case == "null_ws" else ctypes.c_void_p(0x20000 + (16 if case == "misaligned_ws" else 0))
