@@ -720,8 +720,10 @@ def sweep(args):
     #      hiddens drawn on the device with the layer recipe's ranges (timing
     #      only).  "outputs": a layer whose output feeds the next layer of the
     #      group; "state only": the group's last layer (no q, z or output path,
-    #      no feed-forward block).  Per-stage times from the library's stage
-    #      events; the projections are priced against the bf16 MFMA peak.
+    #      no feed-forward block).  "us": an eager call; "us_graph" (and
+    #      tokens_per_s): the call replayed from a HIP graph, without host
+    #      overhead.  Per-stage times from the library's stage events; the
+    #      projections are priced against the bf16 MFMA peak.
     if want("block"):
         D, hk, hv, d = 2048, 16, 32, 128
         cq, cv = hk * d, hv * d
@@ -751,6 +753,15 @@ def sweep(args):
                                                        outputs=outputs, act_dtype=act, state_out=st, out=out,
                                                        workspace=ws, events=ev)
             t = timed_us(call)
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                call()
+            torch.cuda.current_stream().wait_stream(side)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                call()
+            t_graph = timed_us(graph.replay)
             names = gdn.la_block_stage_names(outputs)
             per = {n: [] for n in names}
             for _ in range(reps):
@@ -764,7 +775,8 @@ def sweep(args):
             fl_in = 2.0 * T * D * rows
             rec = {"workload": f"LA layer replay D={D} Hk={hk} Hv={hv} d={d}, {label}, "
                                f"{'outputs' if outputs else 'state only'}, {act} intermediates",
-                   "tokens": T, "us": t["p50"], "tokens_per_s": T / (t["p50"] * 1e-6),
+                   "tokens": T, "us": t["p50"], "us_graph": t_graph["p50"],
+                   "tokens_per_s": T / (t_graph["p50"] * 1e-6),
                    "stage_us": stages,
                    "in_proj_tflops": fl_in / (stages["in-projection"] * 1e-6) / 1e12,
                    "in_proj_frac_of_bf16_peak": fl_in / (stages["in-projection"] * 1e-6) / 1e12 / BF16_PEAK_TFLOPS}

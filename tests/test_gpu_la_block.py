@@ -178,3 +178,48 @@ def test_two_layer_chain():
     assert e0 <= STATE_TOL
     # layer 1's input differs by the bf16 rounding of out on each side (5e-3 bar)
     assert e1 <= BF16_ACT_TOL
+
+
+@pytest.mark.parametrize("outputs", [True, False])
+def test_block_in_a_graph(outputs):
+    """The whole call captured in a HIP graph (after one eager call has set up
+    the projections) replays bitwise like the eager call, three times, with
+    other eager work on the stream between the replays."""
+    dims = LayerDims(hidden=512, hk=4, hv=8, dk=128, dv=128)
+    x, cu, w = _case(206, dims, [200, 70])
+    xd, wd = _bf16_dev(x), _dev_weights(w)
+    cu_d, cu_h = torch.from_numpy(cu).cuda(), torch.from_numpy(cu.copy())
+    n, T = len(cu) - 1, int(cu[-1])
+    st = torch.empty((n, dims.hv, dims.dk, dims.dv), dtype=torch.float32, device="cuda")
+    out = torch.empty((T, dims.hidden), dtype=torch.bfloat16, device="cuda") if outputs else None
+    ws = torch.empty(gdn.la_block_workspace_size(dims.hidden, dims.hk, dims.hv, dims.dk, dims.dv,
+                                                 cu.tolist(), outputs, "bf16") + 256,
+                     dtype=torch.uint8, device="cuda")
+    call = lambda: gdn.la_block_replay(xd, wd, cu_d, dims.hk, dims.hv, dims.dk, dims.dv, 0.1,
+                                       cu_seqlens_host=cu_h, outputs=outputs, act_dtype="bf16",
+                                       state_out=st, out=out, workspace=ws)
+    call()
+    torch.cuda.synchronize()
+    st_ref = st.clone()
+    out_ref = out.clone() if outputs else None
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        call()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        call()
+    for rep in range(3):
+        st.zero_()
+        if outputs:
+            out.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(st, st_ref), f"replay {rep}: state differs"
+        if outputs:
+            assert torch.equal(out, out_ref), f"replay {rep}: output differs"
+        junk = torch.randn(1 << 20, device="cuda").sum()   # eager work between replays
+        torch.cuda.synchronize()
+        del junk
