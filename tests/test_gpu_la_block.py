@@ -14,7 +14,12 @@ the 5e-3 output bar per sequence.  With bf16 intermediates four more
 roundings sit on the path (P, q/k/v, o, y); each is 2^-9 relative at most,
 about 1.1e-3 rms, and k enters the delta rule twice, so the state error is
 expected near 3-4e-3 (an fp64 simulation of exactly these roundings at the
-full layer shape gives 4.1e-3); those runs are held to 1e-2.
+full layer shape gives 4.1e-3); those runs are held to 1e-2.  Their outputs
+are held to 1e-2 per sequence of at least 16 tokens and over the whole batch:
+a sequence of one token outputs scale beta v (k . q), a single dot product of
+bf16-rounded unit vectors whose relative error grows as 1 / |k . q| (1.3e-2
+measured for one such token), and the gated RMS norm carries that relative
+error into y unchanged; longer sequences average it out.
 """
 import numpy as np
 import pytest
@@ -72,12 +77,13 @@ def _gpu_run(x, cu, w, dims, scale, outputs, act, out=None):
     return st, o
 
 
-def out_err(got, want, cu):
-    """max over sequences of ||got - want||_F / ||want||_F over the [len, D] block."""
+def out_err(got, want, cu, min_len=1):
+    """max over sequences (of at least min_len tokens) of ||got - want||_F /
+    ||want||_F over the [len, D] block."""
     worst = 0.0
     for n in range(len(cu) - 1):
         a, b = int(cu[n]), int(cu[n + 1])
-        if a == b:
+        if b - a < min_len:
             continue
         den = np.linalg.norm(want[a:b])
         worst = max(worst, np.linalg.norm(got[a:b] - want[a:b]) / den)
@@ -91,8 +97,13 @@ def _check(name, x, cu, w, dims, scale, outputs, act):
     tol_s = STATE_TOL if act == "f32" else BF16_ACT_TOL
     msg = f"[la_block] {name} act={act} outputs={outputs}: state={e_st:.3e}"
     if outputs:
-        e_o = out_err(to_f64(o), wo, cu)
-        msg += f" out={e_o:.3e}"
+        got = to_f64(o)
+        if act == "f32":
+            e_o = out_err(got, wo, cu)
+        else:
+            e_o = max(out_err(got, wo, cu, min_len=16),
+                      np.linalg.norm(got - wo) / np.linalg.norm(wo) if len(wo) else 0.0)
+        msg += f" out={e_o:.3e} (all sequences: {out_err(got, wo, cu):.3e})"
     print(msg, flush=True)
     assert e_st <= tol_s
     if outputs:
