@@ -62,14 +62,21 @@ struct IntraLds {
   static constexpr int KP = DK + 8;                 // padded LDS row (bf16 elements)
   static constexpr int NL = kSplit ? 2 : 1;         // hi (and lo) copies
   static constexpr int AP = kChunk + 4;             // fp32 row pitch of A, T and P
-  alignas(16) uint16_t Ks[NL][kChunk][KP];
+  // The per-wave block scratch of the off-diagonal inverse steps takes the
+  // keys' place: the last key reads (the K record) end before those steps.
+  // Without it the tail-replay variant (bf16, d_k = 128) needs 57.6 KiB and
+  // two workgroups fit on a CU; with it 53.3 KiB, and three fit.
+  union {
+    alignas(16) uint16_t Ks[NL][kChunk][KP];
+    alignas(16) float Ys[4][16][17];
+  };
   alignas(16) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
   alignas(16) float As[kChunk][AP];                 // A (strictly lower)
   alignas(16) float Ts[kChunk][AP];                 // T = (I + A)^-1
   alignas(16) float Ps[FWD ? kChunk : 1][AP];
-  alignas(16) float Ys[4][16][17];                  // per-wave block scratch
   alignas(16) float Gs[kChunk];
   alignas(16) float Bs[kChunk];
+  static_assert(sizeof(float[4][16][17]) <= sizeof(uint16_t[NL][kChunk][KP]), "block scratch fits in the keys");
 };
 
 // One intra workgroup (256 threads) for chunk slot `slot` and value head `h`,
