@@ -66,14 +66,18 @@ struct IntraLds {
   // keys' place: the last key reads (the K record) end before those steps.
   // Without it the tail-replay variant (bf16, d_k = 128) needs 57.6 KiB and
   // two workgroups fit on a CU; with it 53.3 KiB, and three fit.
+  // Likewise P takes the queries' place: it stays in registers until the Q
+  // record is written (the forward variant: 87.5 -> 70 KiB, two per CU).
   union {
     alignas(16) uint16_t Ks[NL][kChunk][KP];
     alignas(16) float Ys[4][16][17];
   };
-  alignas(16) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
+  union {
+    alignas(16) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
+    alignas(16) float Ps[FWD ? kChunk : 1][AP];
+  };
   alignas(16) float As[kChunk][AP];                 // A (strictly lower)
   alignas(16) float Ts[kChunk][AP];                 // T = (I + A)^-1
-  alignas(16) float Ps[FWD ? kChunk : 1][AP];
   alignas(16) float Gs[kChunk];
   alignas(16) float Bs[kChunk];
   static_assert(sizeof(float[4][16][17]) <= sizeof(uint16_t[NL][kChunk][KP]), "block scratch fits in the keys");
@@ -153,8 +157,9 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   // ---- K K^T (and Q K^T) on MFMA, 10 lower tiles over 4 waves (tiles wave,
   //      wave + 4, wave + 8), turned into A (and P).  All operand reads first,
   //      then the MFMAs, then the elementwise pass.
+  constexpr int TPW = 3;   // tiles of K K^T per wave, at most
+  f32x4 pkeep[TPW];        // this wave's tiles of P until the queries are dead
   {
-    constexpr int TPW = 3;   // tiles per wave, at most
     Frag fa[TPW][NK], fb[TPW][NK], fq[TPW][NK];
     f32x4 acc[TPW], accq[TPW];
     auto tile_rc = [](int t, int& bi, int& bj) __attribute__((always_inline)) {
@@ -215,7 +220,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
           const int i = 16 * bi + 4 * lg + r;
           const float decay = j <= i ? __expf(gi[r] - gj) : 0.f;
           As[i][j] = j < i ? bi4[r] * decay * acc[u][r] : 0.f;
-          if constexpr (FWD) Ps[i][j] = scale * decay * accq[u][r];
+          if constexpr (FWD) pkeep[u][r] = scale * decay * accq[u][r];
         }
       }
     }
@@ -301,6 +306,20 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
     }
   }
   __syncthreads();
+
+  if constexpr (FWD) {
+    // the Q record is written: P goes where the queries were
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+      const int t = wave + 4 * u;
+      if (t < 10) {
+        const int bi = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
+        const int bj = t - bi * (bi + 1) / 2;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Ps[16 * bi + 4 * lg + r][16 * bj + lr] = pkeep[u][r];
+      }
+    }
+  }
 
   // ---- off-diagonal blocks by the block-inverse identity for a lower block
   //      triangular matrix: inv([[I + A11, 0], [A21, I + A22]]) has lower-left
