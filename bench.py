@@ -186,10 +186,10 @@ def summarize_pmc(fetch_dir, write_dir, replay, out_path=None, workload=None):
                "kernels": kernels,
                "commands": [
                    "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE "
-                   "--output-format csv -d $ROOT/gpurun_out/pmc_fetch -o fetch -- python3 $ROOT/bench.py "
+                   "--output-format csv -d $OUT/pmc_fetch -o fetch -- python3 $ROOT/bench.py "
                    "--no-cpu-baseline --no-graph --steps 5 --warmup 2 --cold-reps 0 --calib-copy",
-                   "(same with WRITE_SIZE into $ROOT/gpurun_out/pmc_write)",
-                   f"python bench.py --summarize-pmc gpurun_out/pmc_fetch gpurun_out/pmc_write"]}
+                   "(same with WRITE_SIZE into $OUT/pmc_write)",
+                   f"python bench.py --summarize-pmc $OUT/pmc_fetch $OUT/pmc_write"]}
     path = out_path or TRAFFIC_FILE.format(r=replay)
     with open(path, "w") as f:
         json.dump(summary, f, indent=1)
@@ -221,9 +221,9 @@ def main():
         sweep(args)
         return
     if args.gpus != 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path "
-              "(the per-(sequence, head) work shards with no exchange; see DESIGN.md)",
-              file=sys.stderr)
+        print("bench.py measures one GPU and has no multi-GPU path: the (sequence, head) "
+              "units are independent, so several GPUs would each take a share of them with "
+              "no exchange; run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
