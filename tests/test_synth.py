@@ -61,3 +61,25 @@ def test_workload3_draw_is_fixed():
     assert all(Fraction(1, 20) <= r <= Fraction(1, 10) for _, r, _ in d)
     assert all(128 <= s <= 2048 for _, _, s in d)
     assert d == workloads.workload3_draw()
+
+
+def test_layer_hiddens_tail_is_a_slice_and_weights_are_fixed():
+    from synth.layer import LayerDims, exact_weights, hiddens, layer_weights, pack_hiddens
+    full = hiddens(5, 0, 3, 0, 200, 64)
+    tail = hiddens(5, 0, 3, 130, 200, 64)
+    assert full.dtype == np.uint16 and np.array_equal(full[130:], tail)
+    assert not np.array_equal(hiddens(5, 1, 3, 130, 200, 64), tail)   # another layer
+    dims = LayerDims(hidden=64, hk=2, hv=4, dk=16, dv=8)
+    w1, w2 = layer_weights(5, 0, dims), layer_weights(5, 0, dims)
+    for name in w1:
+        assert np.array_equal(w1[name], w2[name])
+    assert w1["w_in"].shape == (dims.in_rows, 64) and w1["w_in"].dtype == np.uint16
+    assert w1["w_out"].shape == (64, dims.cv) and w1["conv_w"].shape == (2 * dims.cq + dims.cv, 4)
+    ex = exact_weights(w1)
+    # the gate parameters land where the recipe puts them: A = exp(A_log) in [1, 16],
+    # softplus(dt_bias) = dt in [1e-3, 1e-1]
+    assert np.all((np.exp(ex["a_log"]) >= 1 - 1e-6) & (np.exp(ex["a_log"]) <= 16 + 1e-5))
+    dt = np.logaddexp(0.0, ex["dt_bias"])
+    assert np.all((dt > 0.99e-3) & (dt < 1.01e-1))
+    x, cu = pack_hiddens([hiddens(5, 0, i, 0, n, 64) for i, n in enumerate([3, 0, 70])], 64)
+    assert list(cu) == [0, 3, 3, 73] and x.shape == (73, 64)
