@@ -44,7 +44,9 @@
  * with two additions: the first call on a device creates that device's
  * hipBLASLt handle, kept until the process ends (the projections run through
  * hipBLASLt; their workspace is part of the caller's), and `out` may alias
- * `x` (x is read only by the in-projection, before out is written).
+ * `x` (x is read only by the in-projection, before out is written).  To
+ * capture calls in a HIP graph, make one eager call of the same shape first
+ * (the handle and the projections' algorithm choice are set up on it).
  * Requirements: D % 8 == 0, Hv % 4 == 0, d_k and d_v in {64, 128}, Hv % Hk == 0,
  * conv_taps == 4; x, w_in, w_out, out, conv_w and norm_w 16-byte aligned; workspace
  * 256-byte aligned.

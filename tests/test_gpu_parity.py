@@ -203,3 +203,45 @@ def test_workload4_full_prefill_and_tails_sampled(gate_scale):
     _report(f"workload4 s={gate_scale} full 32K + tails (sampled)", full_state=e_st,
             full_out=e_o, tails=e_tail)
     assert e_st <= STATE_TOL and e_o <= OUTPUT_TOL and e_tail <= STATE_TOL
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_random_configurations(seed):
+    """Fixed-seed random configurations of every call with a state or output:
+    1-12 sequences of 0-400 tokens (empty and one-token sequences included by
+    chance and by force), d_k, d_v in {64, 128}, 1-4 value heads per key head,
+    bf16 or fp32, tail replay, forward from a random state and the fused call."""
+    rng = np.random.default_rng(1000 + seed)
+    dk, dv = int(rng.choice([64, 128])), int(rng.choice([64, 128]))
+    hk = int(rng.integers(1, 4))
+    grp = int(rng.choice([1, 2, 4]))
+    dtype = "bf16" if rng.random() < 0.7 else "f32"
+    shape = synth.Shape(hk=hk, hv=hk * grp, dk=dk, dv=dv, dtype=dtype)
+    n = int(rng.integers(1, 13))
+    lens = [int(x) for x in rng.integers(0, 401, n)]
+    lens[int(rng.integers(0, n))] = int(rng.choice([0, 1, 64]))
+    gate = float(rng.choice([0.02, 0.1, 0.5]))
+    tail = synth.pack([synth.tokens(300 + seed, 0, i, 0, L, shape, gate) for i, L in enumerate(lens)], shape)
+    suf_lens = [int(x) for x in rng.integers(0, 200, n)]
+    suf = synth.pack([synth.tokens(300 + seed, 0, i, L, L + s, shape, gate)
+                      for i, (L, s) in enumerate(zip(lens, suf_lens))], shape)
+    xt, xs = device_inputs(tail), device_inputs(suf)
+    scale = dk ** -0.5
+    st = gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"])
+    _, want_st = oracle_run(tail)
+    e_tail = state_err(to_f64(st), want_st)
+    s0 = (rng.standard_normal((n, shape.hv, dk, dv)) * 0.2).astype(np.float32)
+    o, st2 = gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
+                               state_in=torch.from_numpy(s0).cuda(), scale=scale)
+    want_o, want_st2 = oracle_run(suf, state_in=s0.astype(np.float64), outputs=True, scale=scale)
+    e_fwd, e_out = state_err(to_f64(st2), want_st2), output_err(to_f64(o), want_o, suf.cu_seqlens)
+    o3, mid, fin = gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xs["q"], xs["k"],
+                                      xs["v"], xs["g"], xs["beta"], xs["cu"], cu_tail_host=xt["cu_host"],
+                                      cu_suf_host=xs["cu_host"], scale=scale)
+    want_o3, want_fin = oracle_run(suf, state_in=want_st, outputs=True, scale=scale)
+    e_mid, e_fin = state_err(to_f64(mid), want_st), state_err(to_f64(fin), want_fin)
+    e_out3 = output_err(to_f64(o3), want_o3, suf.cu_seqlens)
+    _report(f"random {seed}: N={n} {dtype} dk={dk} dv={dv} hk={hk} grp={grp} gate={gate}",
+            tail=e_tail, fwd=e_fwd, out=e_out, mid=e_mid, fin=e_fin, out3=e_out3)
+    assert max(e_tail, e_fwd, e_mid, e_fin) <= STATE_TOL
+    assert max(e_out, e_out3) <= OUTPUT_TOL
