@@ -99,8 +99,9 @@ gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, co
 }
 
 // The column-split scan has the shortest chunk latency but one workgroup per
-// CU; it is used when its grid fits on the chip at once, else the whole-head
-// scan (4x the columns per CU, two waves per SIMD).
+// CU; it is used when its grid fits on the chip at once.  Otherwise tail
+// replay of bf16 inputs takes the 64-wide column scan (the same chunk latency,
+// twice the columns per CU) and everything else the whole-head scan.
 gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -122,10 +123,15 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
   uint32_t col_groups = 0;
   gdn_status st = cols_fit(s, &fits, &col_groups);
   if (st != GDN_OK) return st;
+  constexpr bool kWide = !FWD && sizeof(TIn) == 2;   // tail replay, bf16 inputs
   if (fits) {
     hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0, stream, cu,
                        s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, Pw,
                        state_in, static_cast<TIn*>(o), state_out);
+  } else if constexpr (kWide) {
+    const uint32_t wide_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kColsWide);
+    hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK>), dim3(wide_groups), dim3(cols_wide_threads()), 0, stream, cu,
+                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, state_out);
   } else {
     hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
                        dim3(head_threads(DV)), 0, stream, cu, s.num_k_heads, s.num_v_heads,

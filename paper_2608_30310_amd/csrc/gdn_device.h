@@ -29,6 +29,20 @@ __device__ __forceinline__ int xcd_remap(int b, int total) {
   return x < rem ? x * (per + 1) + i : rem * (per + 1) + (x - rem) * per + i;
 }
 
+// The same for a grid of clusters of `cs` consecutive logical units (total a
+// multiple of cs): each cluster goes whole to one XCD (its units share records
+// in that XCD's L2) and consecutive clusters go to consecutive XCDs, so every
+// XCD gets an even share of every part of the grid; a varlen batch's long
+// sequences are spread over all XCDs instead of landing on one.  Clusters past
+// the last full round of kXcds fall back to xcd_remap.  A bijection on
+// [0, total).
+__device__ __forceinline__ int xcd_cluster_remap(int b, int total, int cs) {
+  const int full = total / (kXcds * cs) * (kXcds * cs);
+  if (b >= full) return full + xcd_remap(b - full, total - full);
+  const int x = b % kXcds, i = b / kXcds;
+  return (kXcds * (i / cs) + x) * cs + i % cs;
+}
+
 // Barrier for data exchanged through LDS: waits for this wave's LDS accesses
 // only (not for its outstanding global loads, DMA or stores, as
 // __syncthreads does), and keeps the compiler from moving memory accesses

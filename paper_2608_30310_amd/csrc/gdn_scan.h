@@ -462,13 +462,23 @@ constexpr int kColsPerGroup = 32;
 constexpr bool cols_dma_wave(bool fwd, bool split) { return fwd && !split; }
 constexpr int cols_threads(bool fwd, bool split) { return (fwd ? (split ? 4 : 5) : 3) * kWave; }
 
-template <typename TIn, int DK, bool FWD>
-using ColsLds = ScanLds<TIn, DK, kColsPerGroup, FWD, true>;
+template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup>
+using ColsLds = ScanLds<TIn, DK, COLS, FWD, true>;
 
-// One column-split workgroup (block `block` of `nblocks`), LDS in `lds`.
-// Waves 0 and 1 compute, wave 2 issues the DMA; any further waves of the
-// workgroup only take part in the barriers.
-template <typename TIn, int DK, bool FWD>
+// Tail replay without outputs also comes 64 columns wide: four compute waves,
+// one per SIMD, and a DMA wave.  A wave's chunk takes as long as in the 32-wide
+// workgroup (each SIMD still runs one chain), so a CU advances twice the
+// columns per chunk: the choice for grids that do not fit on the chip at once
+// (a 64-wide workgroup moves 52 KiB of records and values per chunk for 64
+// columns; the whole-head kernel's eight waves each read 44 KiB of them from
+// LDS for 128 columns and are held back by it).
+constexpr int kColsWide = 64;
+constexpr int cols_wide_threads() { return (kColsWide / 16 + 1) * kWave; }
+
+// One column-split workgroup (block `block` of `nblocks`), LDS in `lds`, COLS
+// columns per workgroup.  Waves 0 .. COLS/16 - 1 compute, the next issues the
+// DMA; any further waves of the workgroup only take part in the barriers.
+template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup>
 __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int nblocks,
                                                const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                                int32_t dv, const TIn* __restrict__ v,
@@ -476,19 +486,20 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
                                                const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                const float* __restrict__ state_in, TIn* __restrict__ o,
                                                float* __restrict__ state_out) {
-  using L = ColsLds<TIn, DK, FWD>;
+  using L = ColsLds<TIn, DK, FWD, COLS>;
   constexpr int NT = DK / 16;
+  constexpr int CW = COLS / 16;   // compute waves
   const int tid = threadIdx.x;
   // wave index made provably uniform: DMA destinations (M0) stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const bool data_wave = wave >= 2;
-  const bool dma_wave = wave == 2;
+  const bool data_wave = wave >= CW;
+  const bool dma_wave = wave == CW;
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
-  const int ngroups = dv / kColsPerGroup;
+  const int ngroups = dv / COLS;
   // logical unit: the column groups of a value head, then the value heads of a
-  // key head, are adjacent (same XCD, shared records in its L2)
-  const int unit = xcd_remap(block, nblocks);
-  const int col0 = kColsPerGroup * (unit % ngroups);
+  // key head, are adjacent and one cluster (same XCD, shared records in its L2)
+  const int unit = xcd_cluster_remap(block, nblocks, ngroups * (hv / hk));
+  const int col0 = COLS * (unit % ngroups);
   const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
   const int col = col0 + 16 * wave + lr;
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
@@ -607,8 +618,8 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
   const int ngroups = dv / kColsPerGroup;
   // logical unit: the column groups of a value head, then the value heads of a
-  // key head, are adjacent (same XCD, shared records in its L2)
-  const int unit = xcd_remap(block, nblocks);
+  // key head, are adjacent and one cluster (same XCD, shared records in its L2)
+  const int unit = xcd_cluster_remap(block, nblocks, ngroups * (hv / hk));
   const int col0 = kColsPerGroup * (unit % ngroups);
   const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
   const int colw = col0 + 16 * tile;
@@ -782,6 +793,18 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   }
 }
 
+// The 64-wide column scan, tail replay only (grid N x Hv x d_v / 64).
+template <typename TIn, int DK>
+__global__ __launch_bounds__(cols_wide_threads())
+void k_scan_cols_wide(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
+                      const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                      const float* __restrict__ Sw, float* __restrict__ state_out) {
+  using L = ColsLds<TIn, DK, false, kColsWide>;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+  scan_cols_body<TIn, DK, false, kColsWide>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw,
+                                            Sw, nullptr, nullptr, nullptr, state_out);
+}
+
 // ---------------------------------------------------------------- replay scan + suffix intra
 // One launch, two kinds of workgroup (256 threads): blocks [0, n_scan) run the
 // column-split tail replay (FWD = false, zero start, final state to
@@ -836,8 +859,8 @@ void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
-  // logical unit: the value heads of a key head are adjacent (same XCD)
-  const int unit = xcd_remap(blockIdx.x, gridDim.x);
+  // logical unit: the value heads of a key head are adjacent and one cluster (same XCD)
+  const int unit = xcd_cluster_remap(blockIdx.x, gridDim.x, hv / hk);
   const ScanUnit u = scan_unit(cu, unit / hv, unit % hv, hv, hk);
   const int col = 16 * wave + lr;
   const int64_t vrow = static_cast<int64_t>(hv) * DV;

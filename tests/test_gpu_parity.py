@@ -60,7 +60,9 @@ def test_ragged_varlen(dtype, dk, dv, grp):
 
 
 # 72 short sequences: with 4 value heads the column-split grid is 72 x 4 x d_v/32
-# >= 576 workgroups, more than the 256 CUs, so the whole-head scan kernel runs
+# >= 576 workgroups, more than the 256 CUs, so the forward runs on the
+# whole-head scan kernel, and so does the fp32 tail replay; the bf16 tail
+# replay runs on the 64-wide column scan (d_v = 64: one group per head)
 WIDE_LENS = [1 + (37 * i) % 200 for i in range(72)]
 
 
