@@ -45,6 +45,7 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 CHUNK = 64
 CALIB_BYTES = 1 << 30          # plain copy used to calibrate the PMC byte counters (> the 256 MB MALL)
 FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
+QUEUE_SPIN_CYCLES = 2_000_000  # spin kernel that outlasts the host's enqueue of one call
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload1_r{r}.json")
 KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
                   "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
@@ -358,6 +359,23 @@ def main():
                                         "median_us": statistics.median(d)}
     warm = quantiles([ev_t[i][0].elapsed_time(ev_t[i][-1]) * 1e3 for i in range(K)])
 
+    # ---- the same with the call's launches already queued: a spin kernel
+    # holds the GPU while the host enqueues the call, so the interval is the
+    # device's alone (kernels and the gaps between them, no host pacing)
+    def queued(fn):
+        lat = []
+        for _ in range(K):
+            torch.cuda._sleep(QUEUE_SPIN_CYCLES)
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            lat.append(a.elapsed_time(b) * 1e3)
+        return quantiles(lat)
+
+    queued_rebuild = queued(replay_call)
+
     # ---- cold rebuild latency: Infinity Cache flushed before each tail replay
     cold = None
     if args.cold_reps > 0:
@@ -444,6 +462,7 @@ def main():
         "rebuild_latency_us": warm["p50"],
         "rebuild_latency_warm_us": warm,
         "rebuild_latency_cold_us": cold,
+        "rebuild_latency_queued_us": queued_rebuild,
         "replay_tokens_per_s": r / (warm["p50"] * 1e-6),
         "stages": stages,
         "path": {"flops": path_flops, "bytes": path_bytes, "roofline_us": path_bound_s * 1e6,

@@ -99,16 +99,19 @@ gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, co
 }
 
 // The column-split scan has the shortest chunk latency but one workgroup per
-// CU; it is used when its grid fits on the chip at once.  Otherwise tail
-// replay of bf16 inputs takes the 64-wide column scan (the same chunk latency,
-// twice the columns per CU) and everything else the whole-head scan.
-gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups) {
+// CU; it is used when its grid fits on the chip at once.  Tail replay of bf16
+// inputs whose split grid (the two halves of the chain side by side and the
+// second half's transition) also fits runs split, which halves the chain.  When the 32-wide grid does not fit, tail replay of bf16 inputs takes
+// the 64-wide column scan (the same chunk latency, twice the columns per CU)
+// and everything else the whole-head scan.
+gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups, int* cus_out = nullptr) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
     return fail(GDN_ERR_HIP, "querying the device");
   *col_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kColsPerGroup);
   *fits = *col_groups <= static_cast<uint32_t>(cus);
+  if (cus_out) *cus_out = cus;
   return GDN_OK;
 }
 
@@ -121,9 +124,26 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
   const u32x4* Pw = FWD ? reinterpret_cast<const u32x4*>(ws + p.off_P) : nullptr;
   bool fits = false;
   uint32_t col_groups = 0;
-  gdn_status st = cols_fit(s, &fits, &col_groups);
+  int cus = 0;
+  gdn_status st = cols_fit(s, &fits, &col_groups, &cus);
   if (st != GDN_OK) return st;
   constexpr bool kWide = !FWD && sizeof(TIn) == 2;   // tail replay, bf16 inputs
+  if constexpr (kWide) {
+    if (p.split && split_groups(s) <= cus) {
+      // two half-length chains side by side, then state = A state + M''
+      float* m2 = reinterpret_cast<float*>(ws + p.off_M2);
+      float* a2 = reinterpret_cast<float*>(ws + p.off_A2);
+      hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
+                         dim3(cols_wide_threads()), 0, stream, static_cast<int32_t>(split_first_groups(s)), cu,
+                         s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw,
+                         state_out, m2, a2);
+      if ((st = check_launch("split scan launch")) != GDN_OK) return st;
+      hipLaunchKernelGGL((k_state_combine<DK>),
+                         dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCombineCols)),
+                         dim3(kCombineThreads), 0, stream, s.d_v, a2, m2, state_out);
+      return check_launch("state combine launch");
+    }
+  }
   if (fits) {
     hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0, stream, cu,
                        s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, Pw,

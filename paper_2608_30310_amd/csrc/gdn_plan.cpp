@@ -99,6 +99,15 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   off = align_up(off + kSRecordBytes * recs);
   p.off_P = off;
   if (with_outputs) off = align_up(off + kPRecordBytes * recs);
+  p.split = !with_outputs && shape->qkv_dtype == GDN_BF16 && max_chunks >= kSplitMinChunks &&
+            split_groups(*shape) <= kSplitMaxGroups;
+  if (p.split) {
+    const size_t heads = static_cast<size_t>(N) * hv;
+    p.off_M2 = off;
+    off = align_up(off + heads * shape->d_k * shape->d_v * sizeof(float));
+    p.off_A2 = off;
+    off = align_up(off + heads * shape->d_k * shape->d_k * sizeof(float));
+  }
   p.bytes = off;
   *plan = p;
   return GDN_OK;

@@ -54,8 +54,30 @@ struct Plan {
   size_t off_T = 0;               // [num_slots, Hv] T = (I + A)^-1 fragments
   size_t off_S = 0;               // [num_slots, Hv] row scalars
   size_t off_P = 0;               // [num_slots, Hv] P fragments (outputs only)
+  // Tail replay in two halves (see split_groups): the second half's state
+  // from zero and its transition, fp32
+  bool split = false;
+  size_t off_M2 = 0;              // [N, Hv, d_k, d_v]
+  size_t off_A2 = 0;              // [N, Hv, d_k, d_k]
   size_t bytes = 0;               // total workspace size
 };
+
+// Tail replay of bf16 inputs may run as two half-length scans and a combine
+// when every workgroup of the split grid fits on the chip at once (one per CU):
+// N x Hv x (d_v / 32 + (d_v + d_k) / 64) of them, at most kSplitMaxGroups (the
+// MI355X's 256 CUs; fewer on a smaller device are checked at launch), and
+// the longest sequence has at least kSplitMinChunks chunks.  Measured on
+// MI355X: one chain of n chunks takes ~1.63 n + 2 us, the split ~1.06 n + 9.4
+// (its chunks are slower with every CU busy, and the combine with the kernel
+// boundary before it costs ~7 us), even at n = 13 and ahead beyond.
+constexpr int64_t kSplitMaxGroups = 256;
+constexpr int32_t kSplitMinChunks = 20;
+inline int64_t split_first_groups(const gdn_shape& s) {
+  return static_cast<int64_t>(s.num_seqs) * s.num_v_heads * (s.d_v / 32);
+}
+inline int64_t split_groups(const gdn_shape& s) {
+  return split_first_groups(s) + static_cast<int64_t>(s.num_seqs) * s.num_v_heads * ((s.d_v + s.d_k) / 64);
+}
 
 // ---------------------------------------------------------------- layer block
 // Workspace the two projections may use (hipBLASLt's split-k kernels).

@@ -475,61 +475,129 @@ using ColsLds = ScanLds<TIn, DK, COLS, FWD, true>;
 constexpr int kColsWide = 64;
 constexpr int cols_wide_threads() { return (kColsWide / 16 + 1) * kWave; }
 
+// Tail replay in two halves: the recurrence over a chunk is affine in the
+// state, M1 = A_c M0 + B_c with A_c = e^{G_last} I - K^T diag(e^{G_last - G}) T
+// diag(beta e^G) K (d_k x d_k), so the state after chunks [0, n) from zero is
+// A M' + M'' where M' is the state after the first c1 chunks, M'' the state
+// after the remaining chunks started from zero, and A the product of their
+// A_c: the same recurrence run with V = 0 from M0 = I.  The parts run side by
+// side in one launch (k_scan_cols_split):
+//   first half  (kFirstHalf):  chunks [0, c1), zero start, state -> state_out
+//   second half (kSecondHalf): chunks [c1, n), zero start, state -> m2, and
+//                              identity start with V = 0, d_k columns -> a2
+// and k_state_combine forms A M' + M'' in state_out.  Each part is the
+// unsplit scan's arithmetic on its chunks.  The first half runs 32 columns
+// per workgroup (~1.9 us per chunk on MI355X with every CU busy), the second
+// 64 (~2.4 us: four waves read the chunk's operands from LDS), so the first
+// half takes the first round(n x 2.4 / 4.3) chunks.
+enum ScanPart { kWhole = 0, kFirstHalf = 1, kSecondHalf = 2 };
+struct SplitOut {
+  float* m2;   // [N, Hv, d_k, d_v] second half from zero
+  float* a2;   // [N, Hv, d_k, d_k] second half's transition, transposed (A^T)
+};
+__device__ __forceinline__ int split_point(int nch) { return (24 * nch + 21) / 43; }
+
 // One column-split workgroup (block `block` of `nblocks`), LDS in `lds`, COLS
 // columns per workgroup.  Waves 0 .. COLS/16 - 1 compute, the next issues the
 // DMA; any further waves of the workgroup only take part in the barriers.
-template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup>
+template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup, int PART = kWhole>
 __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int nblocks,
                                                const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                                int32_t dv, const TIn* __restrict__ v,
                                                const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                                                const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                const float* __restrict__ state_in, TIn* __restrict__ o,
-                                               float* __restrict__ state_out) {
+                                               float* __restrict__ state_out, SplitOut split = {}) {
   using L = ColsLds<TIn, DK, FWD, COLS>;
+  constexpr bool SPLIT = PART != kWhole;
+  static_assert(!(SPLIT && FWD), "the split form is tail replay only");
   constexpr int NT = DK / 16;
   constexpr int CW = COLS / 16;   // compute waves
+  constexpr int kVJob0 = L::kKJobs + L::kTJobs + L::kPJobs;   // first V job
   const int tid = threadIdx.x;
   // wave index made provably uniform: DMA destinations (M0) stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const bool data_wave = wave >= CW;
   const bool dma_wave = wave == CW;
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
-  const int ngroups = dv / COLS;
+  const int ngroups = PART == kSecondHalf ? dv / COLS + DK / COLS : dv / COLS;
   // logical unit: the column groups of a value head, then the value heads of a
   // key head, are adjacent and one cluster (same XCD, shared records in its L2)
   const int unit = xcd_cluster_remap(block, nblocks, ngroups * (hv / hk));
-  const int col0 = COLS * (unit % ngroups);
   const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
+  // this workgroup's chunks [cb, ce), columns, start and destination
+  int g = unit % ngroups, cb = 0, ce = u.nch, ld = dv;
+  bool ident = false;
+  float* dst = state_out;
+  if constexpr (PART == kFirstHalf) {
+    ce = split_point(u.nch);
+  } else if constexpr (PART == kSecondHalf) {
+    cb = split_point(u.nch);
+    if (g < dv / COLS) {
+      dst = split.m2;
+    } else {
+      g -= dv / COLS;
+      ident = true;
+      ld = DK;
+      dst = split.a2;
+    }
+  }
+  const int col0 = COLS * g;
   const int col = col0 + 16 * wave + lr;
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
   auto dma_chunk = [&](int ci, int b) __attribute__((always_inline)) {
-    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, ident ? 0 : col0, v, Kw, Tw, Sw, Pw);
 #pragma unroll
-    for (int j = 0; j < L::kJobs; ++j) dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
+    for (int j = 0; j < L::kJobs; ++j) {
+      // the transition's value rows are the zeros written below
+      if (SPLIT && ident && j >= kVJob0 && j < kVJob0 + L::kVJobs) continue;
+      dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
+    }
   };
 
   f32x4 M[NT];
   Frag mb[DK / 32];
   f32x4 pout[4];
-  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * dv + col;
-  if (!data_wave) load_state<DK>(state_in, sbase, dv, lg, M, mb);
+  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * ld + col;
+  if constexpr (SPLIT) {
+    if (ident) {
+      // M0 = identity columns; V tiles of both buffers zero
+      if (!data_wave) {
+#pragma unroll
+        for (int td = 0; td < NT; ++td)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) M[td][r] = (16 * td + 4 * lg + r == col) ? 1.f : 0.f;
+#pragma unroll
+        for (int kk = 0; kk < DK / 32; ++kk) mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
+      }
+      for (int b = 0; b < L::kBuffers; ++b)
+        for (int x = 16 * tid; x < L::kVBytes; x += 16 * static_cast<int>(blockDim.x))
+          *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(lds_l + b * L::kBytes + L::kOffV + x) =
+              u32x4{0u, 0u, 0u, 0u};
+    } else if (!data_wave) {
+      load_state<DK>(nullptr, sbase, ld, lg, M, mb);
+    }
+  } else {
+    if (!data_wave) load_state<DK>(state_in, sbase, dv, lg, M, mb);
+  }
 
-  if (dma_wave && u.nch > 0) {
-    dma_chunk(0, 0);
+  const int nch = ce - cb;
+  if (dma_wave && nch > 0) {
+    dma_chunk(cb, 0);
     wait_dma();
   }
   __syncthreads();
-  for (int ci = 0; ci < u.nch; ++ci) {
-    const int b = L::kBuffers == 2 ? (ci & 1) : 0;
+  for (int j = 0; j < nch; ++j) {
+    const int ci = cb + j;
+    const int b = L::kBuffers == 2 ? (j & 1) : 0;
     if (data_wave) {
-      if (dma_wave && L::kBuffers == 2 && ci + 1 < u.nch) {
+      if (dma_wave && L::kBuffers == 2 && j + 1 < nch) {
         dma_chunk(ci + 1, b ^ 1);   // lands while the compute waves work on buffer b
         wait_dma();
       }
     } else {
       if constexpr (FWD) {
-        if (ci > 0) store_chunk_out(o, u, ci - 1, hv, dv, col - lr, lane, pout);
+        if (j > 0) store_chunk_out(o, u, ci - 1, hv, dv, col - lr, lane, pout);
       }
       const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
       chunk_step<L, DK, FWD, false>((const unsigned char*)(lds_l + b * L::kBytes), 16 * wave, pg, lane, M, mb,
@@ -537,7 +605,7 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
     }
     if (L::kBuffers == 1) {
       __syncthreads();   // the compute waves are done with the only buffer
-      if (dma_wave && ci + 1 < u.nch) {
+      if (dma_wave && j + 1 < nch) {
         dma_chunk(ci + 1, 0);
         wait_dma();
       }
@@ -546,14 +614,20 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
   }
   if (!data_wave) {
     if constexpr (FWD) {
-      if (u.nch > 0) store_chunk_out(o, u, u.nch - 1, hv, dv, col - lr, lane, pout);
+      if (nch > 0) store_chunk_out(o, u, ce - 1, hv, dv, col - lr, lane, pout);
     }
-    if (state_out) {
+    if (SPLIT && ident) {
+      // the transition goes out transposed, A^T [d_k x d_k]: a lane's four
+      // rows of column `col` are one 16-byte piece of row `col` of A^T
+      float* at = dst + ((static_cast<int64_t>(u.n) * hv + u.h) * DK + col) * DK + 4 * lg;
+#pragma unroll
+      for (int td = 0; td < NT; ++td) *reinterpret_cast<f32x4*>(at + 16 * td) = M[td];
+    } else if (dst) {
 #pragma unroll
       for (int td = 0; td < NT; ++td)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] = M[td][r];
+          dst[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * ld] = M[td][r];
     }
   }
 }
@@ -803,6 +877,94 @@ void k_scan_cols_wide(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, in
   __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
   scan_cols_body<TIn, DK, false, kColsWide>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw,
                                             Sw, nullptr, nullptr, nullptr, state_out);
+}
+
+// Tail replay in two halves, one launch: blocks [0, n_first) run the first
+// half 32 columns wide (grid N x Hv x d_v / 32; waves 3 and 4 only take part
+// in the barriers), the rest the second half and its transition 64 columns
+// wide (N x Hv x (d_v + d_k) / 64).  state_out holds the first half's state
+// until k_state_combine runs.
+template <typename TIn, int DK>
+__global__ __launch_bounds__(cols_wide_threads())
+void k_scan_cols_split(int32_t n_first, const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
+                       const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                       const float* __restrict__ Sw, float* __restrict__ state_out, float* __restrict__ m2,
+                       float* __restrict__ a2) {
+  using L1 = ColsLds<TIn, DK, false, kColsPerGroup>;
+  using L2 = ColsLds<TIn, DK, false, kColsWide>;
+  constexpr int kB1 = L1::kBuffers * L1::kBytes, kB2 = L2::kBuffers * L2::kBytes;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[kB1 > kB2 ? kB1 : kB2];
+  const int b = blockIdx.x;
+  if (b < n_first)
+    scan_cols_body<TIn, DK, false, kColsPerGroup, kFirstHalf>((lds_byte*)lds, b, n_first, cu, hk, hv, dv, v,
+                                                              Kw, Tw, Sw, nullptr, nullptr, nullptr, state_out);
+  else
+    scan_cols_body<TIn, DK, false, kColsWide, kSecondHalf>((lds_byte*)lds, b - n_first,
+                                                           static_cast<int>(gridDim.x) - n_first, cu, hk, hv,
+                                                           dv, v, Kw, Tw, Sw, nullptr, nullptr, nullptr,
+                                                           nullptr, SplitOut{m2, a2});
+}
+
+// state = A state + B per (sequence, value head): A^T [d_k x d_k], state and
+// B [d_k x d_v], fp32 row-major.  grid N x Hv x d_v / 16; a workgroup owns 16
+// whole columns of one state (it reads them all before it writes any) and
+// stages A^T and those columns in LDS, every load in flight at once.  The
+// product runs on fp32 MFMA (16x16x4, fp32 products and sums): wave w takes
+// the 16-row tiles w, w + 4, ..; per 4-step slice of k, lane l supplies
+// A[16 t + l % 16][k + l / 16] (= A^T[k + l / 16][..], one conflict-free LDS
+// read) and column l % 16 of row k + l / 16 of the staged state, and holds
+// D[4 (l / 16) + i][l % 16] of the tile.
+constexpr int kCombineThreads = 256;
+constexpr int kCombineCols = 16;
+template <int DK>
+__global__ __launch_bounds__(kCombineThreads)
+void k_state_combine(int32_t dv, const float* __restrict__ At, const float* __restrict__ B,
+                     float* __restrict__ state) {
+  constexpr int PER = DK * kCombineCols / kCombineThreads;   // staged column values per thread
+  constexpr int AV = DK * DK / 4 / kCombineThreads;          // 16-byte pieces of A^T per thread
+  constexpr int TILES = DK / 16 / (kCombineThreads / kWave);  // row tiles per wave
+  __shared__ __attribute__((aligned(16))) float as[DK * DK];
+  __shared__ __attribute__((aligned(16))) float ms[DK * kCombineCols];
+  const int groups = dv / kCombineCols;
+  const int64_t head = blockIdx.x / groups;
+  const int c0 = kCombineCols * (blockIdx.x % groups);
+  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int li = lane % 16, lk = lane / 16;
+  float* st = state + head * DK * dv + c0;
+  const float* bm = B + head * DK * dv + c0;
+  const f32x4* at = reinterpret_cast<const f32x4*>(At + head * DK * DK);
+  f32x4 av[AV];
+#pragma unroll
+  for (int i = 0; i < AV; ++i) av[i] = at[tid + kCombineThreads * i];
+  float mv[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int x = tid + kCombineThreads * i;
+    mv[i] = st[static_cast<int64_t>(x / kCombineCols) * dv + x % kCombineCols];
+  }
+  f32x4 acc[TILES];
+#pragma unroll
+  for (int t = 0; t < TILES; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      acc[t][i] = bm[static_cast<int64_t>(16 * (wave + 4 * t) + 4 * lk + i) * dv + li];
+#pragma unroll
+  for (int i = 0; i < AV; ++i) reinterpret_cast<f32x4*>(as)[tid + kCombineThreads * i] = av[i];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) ms[tid + kCombineThreads * i] = mv[i];
+  __syncthreads();
+#pragma unroll 4
+  for (int k = 0; k < DK; k += 4) {
+    const float b = ms[(k + lk) * kCombineCols + li];
+#pragma unroll
+    for (int t = 0; t < TILES; ++t)
+      acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(as[(k + lk) * DK + 16 * (wave + 4 * t) + li], b, acc[t],
+                                                    0, 0, 0);
+  }
+#pragma unroll
+  for (int t = 0; t < TILES; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) st[static_cast<int64_t>(16 * (wave + 4 * t) + 4 * lk + i) * dv + li] = acc[t][i];
 }
 
 // ---------------------------------------------------------------- replay scan + suffix intra

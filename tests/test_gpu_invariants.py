@@ -32,6 +32,7 @@ def _seq(seq, n, start=0, shape=SHAPE, gate_scale=0.1):
 
 
 def test_replay_of_whole_prefix_is_full_prefill_bitwise():
+    # below 20 chunks tail replay runs one chain, as the forward does
     p = synth.pack([_seq(0, 333)])
     x = device_inputs(p)
     st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
@@ -220,3 +221,32 @@ def test_replay_forward_equals_the_two_calls_bitwise(case):
     assert torch.equal(mid, st)
     assert torch.equal(of, o)
     assert torch.equal(stf, st2)
+
+
+@pytest.mark.parametrize("r,slow", [(1300, True), (1638, False), (2000, True), (3277, True), (3277, False)])
+def test_split_replay_agrees_with_one_chain(r, slow):
+    """One sequence at 32 heads replays in two halves (the first half's state,
+    the second half's from zero and its transition, combined); the same
+    sequence in a batch of two exceeds the split grid and runs one chain, and
+    so does the fused call's tail.  The three differ by rounding order only.
+    `slow`: gates that decay slowly (scale 0.002, beta x 0.1), so the first
+    half's share of the state is large and the combine is exercised."""
+    import dataclasses
+    shape = synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16")
+    s = synth.tokens(207, 0, 0, 0, r, shape, gate_scale=0.002 if slow else 0.1)
+    if slow:
+        s = dataclasses.replace(s, beta=(s.beta * 0.1).astype(np.float32))
+    x1, x2 = device_inputs(synth.pack([s])), device_inputs(synth.pack([s, s]))
+    split = gdn.tail_replay(x1["k"], x1["v"], x1["g"], x1["beta"], x1["cu"], x1["cu_host"])
+    chain = gdn.tail_replay(x2["k"], x2["v"], x2["g"], x2["beta"], x2["cu"], x2["cu_host"])
+    assert torch.equal(chain[0], chain[1])
+    e = state_err(to_f64(split), to_f64(chain[:1]))
+    xs = device_inputs(synth.pack([synth.tokens(207, 0, 0, r, r + 64, shape)]))
+    # (the suffix only completes the fused call; its outputs are not compared)
+    _, mid, _ = gdn.replay_forward(x1["k"], x1["v"], x1["g"], x1["beta"], x1["cu"],
+                                   xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"],
+                                   cu_tail_host=x1["cu_host"], cu_suf_host=xs["cu_host"])
+    e_mid = state_err(to_f64(mid), to_f64(chain[:1]))
+    print(f"[split] r={r}: split vs one chain {e:.2e}, fused tail vs one chain {e_mid:.2e}", flush=True)
+    assert e <= 1e-5
+    assert torch.equal(mid, chain[:1])

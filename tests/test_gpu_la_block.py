@@ -197,7 +197,8 @@ def test_block_in_a_graph(outputs):
     the projections) replays bitwise like the eager call, three times, with
     other eager work on the stream between the replays."""
     dims = LayerDims(hidden=512, hk=4, hv=8, dk=128, dv=128)
-    x, cu, w = _case(206, dims, [200, 70])
+    # 21 chunks: without outputs the recurrence runs as two halves and a combine
+    x, cu, w = _case(206, dims, [1300, 70])
     xd, wd = _bf16_dev(x), _dev_weights(w)
     cu_d, cu_h = torch.from_numpy(cu).cuda(), torch.from_numpy(cu.copy())
     n, T = len(cu) - 1, int(cu[-1])

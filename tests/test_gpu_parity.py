@@ -87,6 +87,46 @@ def test_wide_batch_whole_head_kernel(dtype, dk, dv):
     assert e_tail <= STATE_TOL and e_st <= STATE_TOL and e_o <= OUTPUT_TOL
 
 
+# Tail replay in two halves: bf16, at least 20 chunks in the longest sequence
+# and N x Hv x 8 <= 256 workgroups (d = 128).  Lengths cover an empty
+# sequence, one token, two chunks (the second half one chunk), 7 chunks and 21
+# with a ragged end, so every part meets a short or empty range somewhere.
+# With the synthetic gates' usual decay the first half's share of the final
+# state is ~1e-7 or less at these lengths and a wrong combine would pass
+# unseen, so these inputs decay slowly (gate scale 0.002, beta x 0.1): the
+# oracle itself shows the first half's share above 10%.
+SPLIT_LENS = [0, 1, 70, 400, 1300]
+
+
+def _slow_decay(t):
+    import dataclasses
+    return dataclasses.replace(t, beta=(t.beta * 0.1).astype(np.float32))
+
+
+@pytest.mark.parametrize("dk,dv", [(64, 64), (128, 128), (64, 128), (128, 64)])
+def test_split_tail_replay_ragged(dk, dv):
+    shape = synth.Shape(hk=2, hv=4, dk=dk, dv=dv, dtype="bf16")
+    seqs = [_slow_decay(synth.tokens(102, 0, i, 0, n, shape, gate_scale=0.002))
+            for i, n in enumerate(SPLIT_LENS)]
+    p = synth.pack(seqs)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    _, want = oracle_run(p)
+    # the longest sequence's second half alone (split point as the kernel takes it)
+    nch = (SPLIT_LENS[-1] + 63) // 64
+    c1 = 64 * ((24 * nch + 21) // 43)
+    t = seqs[-1]
+    import dataclasses
+    second = dataclasses.replace(t, q=t.q[c1:], k=t.k[c1:], v=t.v[c1:], g=t.g[c1:], beta=t.beta[c1:])
+    _, w2 = oracle_run(synth.pack([second]))
+    share = np.linalg.norm(want[-1] - w2[0]) / np.linalg.norm(want[-1])
+    e = state_err(to_f64(st), want)
+    _report(f"split bf16 dk={dk} dv={dv}", tail=e, first_half_share=share)
+    assert share > 0.1
+    assert e <= STATE_TOL
+    assert torch.count_nonzero(st[0]).item() == 0
+
+
 def _chain(shape, hits, outputs_scale=1.0):
     """GPU: tail replay then suffix forward from the rebuilt state; the oracle
     does the same chain in fp64.  Returns the error triple."""
