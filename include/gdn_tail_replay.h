@@ -91,6 +91,13 @@ gdn_status gdn_workspace_size(const gdn_shape* shape,
  *   k [T,Hk,d_k], v [T,Hv,d_v] (qkv_dtype); g, beta [T,Hv] fp32.
  * workspace: device memory of at least gdn_workspace_size(..., 0) bytes,
  * 256-byte aligned; its contents on entry do not matter.
+ * For bf16 inputs whose longest tail has at least 20 chunks and whose batch
+ * is small enough (N x Hv x (d_v / 32 + (d_v + d_k) / 64) workgroups fit on
+ * the device at once), the chain is evaluated in two halves: the state is
+ * linear in the first half's state, so it is formed as the second half's
+ * transition applied to the first half's state plus the second half's state
+ * from zero.  The result equals the one-chain evaluation up to rounding order
+ * (about 1e-6 relative); below those sizes it is the one-chain evaluation.
  */
 gdn_status gdn_tail_replay(const gdn_shape* shape,
                            const int32_t* cu_seqlens_host,
@@ -156,9 +163,11 @@ const char* gdn_stage_name(int32_t with_outputs, int32_t stage);
  * Replay, then continue (paper Section 3: the rebuilt state S_m is the start
  * of the new suffix's prefill, Eq. 2 followed by Eq. 1 from i = m + 1).  One
  * call does what gdn_tail_replay followed by gdn_chunk_forward(state_in =
- * state_mid) does, with the same results bit for bit, but overlaps work that
- * does not depend on the rebuilt state: the suffix's per-chunk preparation
- * runs beside the tail's sequential scan.
+ * state_mid) does, but overlaps work that does not depend on the rebuilt
+ * state: the suffix's per-chunk preparation runs beside the tail's sequential
+ * scan.  The tail always runs as one chain, so the results are bit for bit
+ * those of the two calls wherever gdn_tail_replay runs one chain too, and
+ * equal to rounding order where it splits a long tail in two halves.
  *   tail   (sequence n = the last r_n matched tokens, packed by cu_tail):
  *          k_tail [Tt,Hk,d_k], v_tail [Tt,Hv,d_v], g_tail, beta_tail [Tt,Hv];
  *   suffix (the new tokens of sequence n, packed by cu_suf, same N):
