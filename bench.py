@@ -45,7 +45,8 @@ BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 CHUNK = 64
 CALIB_BYTES = 1 << 30          # plain copy used to calibrate the PMC byte counters (> the 256 MB MALL)
 FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
-QUEUE_SPIN_CYCLES = 2_000_000  # spin kernel that outlasts the host's enqueue of one call
+QUEUE_SPIN_CYCLES = 2_000_000  # spin kernel (~0.8 ms) that outlasts the host's enqueue of one call
+SWEEP_SPIN_CYCLES = 10_000_000  # ~4 ms: outlasts the enqueue of the sweep's longest rep (36 calls)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload1_r{r}.json")
 KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
                   "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
@@ -500,11 +501,15 @@ def sweep(args):
     reps, warm = max(args.steps // 2, 10), 5
 
     def timed_us(fn):
+        # each rep's launches are queued behind a spin kernel before the GPU
+        # reaches its first event: the interval is the device's time (kernels
+        # and the gaps between them), not the host's pacing
         for _ in range(warm):
             fn()
         torch.cuda.synchronize()
         ts = []
         for _ in range(reps):
+            torch.cuda._sleep(SWEEP_SPIN_CYCLES)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             fn()

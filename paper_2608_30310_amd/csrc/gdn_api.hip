@@ -151,10 +151,11 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
   } else if constexpr (kWide) {
     const uint32_t wide_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kColsWide);
     hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK>), dim3(wide_groups), dim3(cols_wide_threads()), 0, stream, cu,
-                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, state_out);
+                       p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw,
+                       state_out);
   } else {
     hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
-                       dim3(head_threads(DV)), 0, stream, cu, s.num_k_heads, s.num_v_heads,
+                       dim3(head_threads(DV)), 0, stream, cu, p.order, s.num_k_heads, s.num_v_heads,
                        static_cast<const TIn*>(v), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o),
                        state_out);
   }

@@ -61,12 +61,15 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   if (!cu) { *err = "cu_seqlens_host is NULL"; return GDN_ERR_NULL_ARG; }
   if (cu[0] != 0) { *err = "cu_seqlens_host[0] must be 0"; return GDN_ERR_BAD_SEQLENS; }
 
-  int64_t chunks = 0, slots = 0;
+  int64_t chunks = 0, slots = 0, prev_c = 0;
   int32_t max_chunks = 0;
+  bool sorted = true;   // chunk counts non-increasing
   for (int32_t n = 0; n < N; ++n) {
     const int64_t len = static_cast<int64_t>(cu[n + 1]) - cu[n];
     if (len < 0) { *err = "cu_seqlens_host must be non-decreasing"; return GDN_ERR_BAD_SEQLENS; }
     const int64_t c = (len + kChunk - 1) / kChunk;
+    if (n > 0 && c > prev_c) sorted = false;
+    prev_c = c;
     chunks += c;
     if (c > 0) slots = std::max(slots, chunk_slot(cu[n], n) + c);
     if (c > max_chunks) max_chunks = static_cast<int32_t>(c);
@@ -99,6 +102,14 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   off = align_up(off + kSRecordBytes * recs);
   p.off_P = off;
   if (with_outputs) off = align_up(off + kPRecordBytes * recs);
+  if (N >= 2 && N <= kMaxOrderedSeqs && !sorted) {
+    int32_t idx[kMaxOrderedSeqs];
+    for (int32_t n = 0; n < N; ++n) idx[n] = n;
+    auto nch = [&](int32_t n) { return (static_cast<int64_t>(cu[n + 1]) - cu[n] + kChunk - 1) / kChunk; };
+    std::stable_sort(idx, idx + N, [&](int32_t a, int32_t b) { return nch(a) > nch(b); });
+    p.order.n = N;
+    for (int32_t n = 0; n < N; ++n) p.order.seq[n] = idx[n];
+  }
   p.split = !with_outputs && shape->qkv_dtype == GDN_BF16 && max_chunks >= kSplitMinChunks &&
             split_groups(*shape) <= kSplitMaxGroups;
   if (p.split) {

@@ -41,6 +41,16 @@ constexpr size_t k_record_bytes(int dk, bool outputs, bool split) {
   return static_cast<size_t>(k_record_frags(dk, outputs)) * (split ? 2 : 1) * kFragBytes;
 }
 
+// Longest-first order of a batch's sequences by chunk count (equal counts keep
+// their index order): seq[r] = the sequence of rank r.  n = 0 means the
+// identity: batches of one sequence, of more than kMaxOrderedSeqs, or whose
+// chunk counts never rise.  Travels by value in a kernel's arguments.
+constexpr int32_t kMaxOrderedSeqs = 256;
+struct SeqOrder {
+  int32_t n = 0;
+  int32_t seq[kMaxOrderedSeqs];
+};
+
 // Where each region lives inside the caller's workspace, and the launch sizes.
 struct Plan {
   int64_t total_tokens = 0;
@@ -54,6 +64,9 @@ struct Plan {
   size_t off_T = 0;               // [num_slots, Hv] T = (I + A)^-1 fragments
   size_t off_S = 0;               // [num_slots, Hv] row scalars
   size_t off_P = 0;               // [num_slots, Hv] P fragments (outputs only)
+  // Longest-first order of the sequences, for scans whose grid exceeds the
+  // chip (passed by value in the kernel's arguments)
+  SeqOrder order;
   // Tail replay in two halves (see split_groups): the second half's state
   // from zero and its transition, fp32
   bool split = false;
@@ -71,6 +84,7 @@ struct Plan {
 // (its chunks are slower with every CU busy, and the combine with the kernel
 // boundary before it costs ~7 us), even at n = 13 and ahead beyond.
 constexpr int64_t kSplitMaxGroups = 256;
+
 constexpr int32_t kSplitMinChunks = 20;
 inline int64_t split_first_groups(const gdn_shape& s) {
   return static_cast<int64_t>(s.num_seqs) * s.num_v_heads * (s.d_v / 32);

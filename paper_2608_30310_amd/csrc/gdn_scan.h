@@ -390,7 +390,13 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
 struct ScanUnit {
   int n, h, kh, tok0, len, slot0, nch;
 };
-__device__ __forceinline__ ScanUnit scan_unit(const int32_t* __restrict__ cu, int n, int h, int hv, int hk) {
+// `slot` is the workgroup's logical sequence slot; `order` (NULL or n = 0:
+// identity) maps it to the sequence, longest first.  When a scan grid exceeds
+// the chip, workgroups start in logical order as earlier ones finish, so a
+// long sequence that comes late in a varlen batch would finish late.
+__device__ __forceinline__ ScanUnit scan_unit(const int32_t* __restrict__ cu, int slot, int h, int hv, int hk,
+                                              const SeqOrder* order = nullptr) {
+  const int n = (order && order->n > 0) ? order->seq[slot] : slot;
   ScanUnit u;
   u.n = n;
   u.h = h;
@@ -507,7 +513,8 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
                                                const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                                                const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                const float* __restrict__ state_in, TIn* __restrict__ o,
-                                               float* __restrict__ state_out, SplitOut split = {}) {
+                                               float* __restrict__ state_out, SplitOut split = {},
+                                               const SeqOrder* order = nullptr) {
   using L = ColsLds<TIn, DK, FWD, COLS>;
   constexpr bool SPLIT = PART != kWhole;
   static_assert(!(SPLIT && FWD), "the split form is tail replay only");
@@ -524,7 +531,7 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
   // logical unit: the column groups of a value head, then the value heads of a
   // key head, are adjacent and one cluster (same XCD, shared records in its L2)
   const int unit = xcd_cluster_remap(block, nblocks, ngroups * (hv / hk));
-  const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
+  const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk, order);
   // this workgroup's chunks [cb, ce), columns, start and destination
   int g = unit % ngroups, cb = 0, ce = u.nch, ld = dv;
   bool ident = false;
@@ -870,13 +877,13 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
 // The 64-wide column scan, tail replay only (grid N x Hv x d_v / 64).
 template <typename TIn, int DK>
 __global__ __launch_bounds__(cols_wide_threads())
-void k_scan_cols_wide(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
+void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
                       const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                       const float* __restrict__ Sw, float* __restrict__ state_out) {
   using L = ColsLds<TIn, DK, false, kColsWide>;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
   scan_cols_body<TIn, DK, false, kColsWide>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw,
-                                            Sw, nullptr, nullptr, nullptr, state_out);
+                                            Sw, nullptr, nullptr, nullptr, state_out, SplitOut{}, &order);
 }
 
 // Tail replay in two halves, one launch: blocks [0, n_first) run the first
@@ -1008,7 +1015,7 @@ constexpr int head_threads(int dv) { return dv / 16 * kWave; }
 
 template <typename TIn, int DK, int DV, bool FWD>
 __global__ __launch_bounds__(head_threads(DV))
-void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
+void k_scan_head(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv,
                  const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                  const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                  const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
@@ -1023,7 +1030,7 @@ void k_scan_head(const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
   // logical unit: the value heads of a key head are adjacent and one cluster (same XCD)
   const int unit = xcd_cluster_remap(blockIdx.x, gridDim.x, hv / hk);
-  const ScanUnit u = scan_unit(cu, unit / hv, unit % hv, hv, hk);
+  const ScanUnit u = scan_unit(cu, unit / hv, unit % hv, hv, hk, &order);
   const int col = 16 * wave + lr;
   const int64_t vrow = static_cast<int64_t>(hv) * DV;
   // jobs wave + W * jj, jj in [j0, j1), of chunk ci into buffer b

@@ -105,6 +105,9 @@ def test_workspace_size_values():
     # two sequences: slots cu[n]/64 + n + j, the last ends at 100/64 + 1 + 1 = 3
     st, n2 = _ws_size(_shape(num_seqs=2), _cu([0, 100, 130]))
     assert st == 0 and n2 == 3 * 32 * (t_rec + s_rec) + 3 * 16 * 32 * frag
+    # the longest-first order travels in the kernels' arguments: no region
+    st, n2u = _ws_size(_shape(num_seqs=2), _cu([0, 30, 130]))
+    assert st == 0 and n2u == 3 * 32 * (t_rec + s_rec) + 3 * 16 * 32 * frag
     # Tail replay of bf16 inputs that may run in two halves (at least 20
     # chunks, N x Hv x (d_v / 32 + (d_v + d_k) / 64) <= 256 workgroups) adds
     # the second half's fp32 state [N, Hv, d_k, d_v] and transition [N, Hv,
