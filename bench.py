@@ -46,7 +46,6 @@ CHUNK = 64
 CALIB_BYTES = 1 << 30          # plain copy used to calibrate the PMC byte counters (> the 256 MB MALL)
 FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
 QUEUE_SPIN_CYCLES = 2_000_000  # spin kernel (~0.8 ms) that outlasts the host's enqueue of one call
-SWEEP_SPIN_CYCLES = 10_000_000  # ~4 ms: outlasts the enqueue of the sweep's longest rep (36 calls)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload1_r{r}.json")
 KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
                   "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
@@ -500,16 +499,18 @@ def sweep(args):
     gdn.load_library()
     reps, warm = max(args.steps // 2, 10), 5
 
-    def timed_us(fn):
-        # each rep's launches are queued behind a spin kernel before the GPU
-        # reaches its first event: the interval is the device's time (kernels
-        # and the gaps between them), not the host's pacing
+    def timed_us(fn, queued=False):
+        # queued: the rep's launches wait behind a spin kernel, so the interval
+        # is the device's time alone (kernels and the gaps between them), not
+        # the host's pacing; otherwise each rep starts from an idle stream and
+        # includes the host's launch latency
         for _ in range(warm):
             fn()
         torch.cuda.synchronize()
         ts = []
         for _ in range(reps):
-            torch.cuda._sleep(SWEEP_SPIN_CYCLES)
+            if queued:
+                torch.cuda._sleep(QUEUE_SPIN_CYCLES)
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             fn()
@@ -583,10 +584,12 @@ def sweep(args):
         wsf, st2, o = buffers(xs, 1, 4, 4, 64, True)
         wsr = fused_ws(xt, xs, 1, 4, 4, 64)
         rep = timed_us(lambda: replay(xt, st, wst))
+        repq = timed_us(lambda: replay(xt, st, wst), queued=True)
         two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
         both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
         emit({"workload": "small fp32 layer Hk=Hv=4 d=64: tail 205 + suffix 256",
-              "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+              "rebuild_latency_us": rep, "rebuild_latency_queued_us": repq,
+              "step_us": both, "step_two_calls_us": two,
               "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
 
     # ---- hybrid-model layer, tail 410 (the default bench line covers 819)
@@ -598,10 +601,12 @@ def sweep(args):
         wsf, st2, o = buffers(xs, 1, 16, 32, 128, True)
         wsr = fused_ws(xt, xs, 1, 16, 32, 128)
         rep = timed_us(lambda: replay(xt, st, wst))
+        repq = timed_us(lambda: replay(xt, st, wst), queued=True)
         two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
         both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
         emit({"workload": "one GDN layer Hk=16 Hv=32 d=128 bf16: tail 410 + suffix 512",
-              "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+              "rebuild_latency_us": rep, "rebuild_latency_queued_us": repq,
+              "step_us": both, "step_two_calls_us": two,
               "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
 
     # ---- 36-layer stack, m = 32768, r = 3277: 36 sequential per-layer replays,
@@ -631,11 +636,13 @@ def sweep(args):
         wsf, st2, o = buffers(xs, n, 16, 32, 128, True)
         wsr = fused_ws(xt, xs, n, 16, 32, 128)
         rep = timed_us(lambda: replay(xt, st, wst))
+        repq = timed_us(lambda: replay(xt, st, wst), queued=True)
         two = timed_us(lambda: (replay(xt, st, wst), forward(xs, st, o, st2, wsf)))
         both = timed_us(lambda: fused(xt, xs, st, o, st2, wsr))
         sr, ss = sum(h.r for h in hits), sum(h.s for h in hits)
         emit({"workload": f"16 varlen hits Hk=16 Hv=32 d=128 bf16: sum r={sr}, sum s={ss}",
-              "rebuild_latency_us": rep, "step_us": both, "step_two_calls_us": two,
+              "rebuild_latency_us": rep, "rebuild_latency_queued_us": repq,
+              "step_us": both, "step_two_calls_us": two,
               "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
               "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
 
