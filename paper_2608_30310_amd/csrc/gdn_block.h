@@ -21,7 +21,8 @@ namespace gdn {
 
 constexpr int kPrepThreads = 256;
 constexpr int kPrepChans = 256;   // channels per prep workgroup (32 threads x 8)
-constexpr int kPrepTokens = kPrepThreads / (kPrepChans / 8);   // 8 tokens per workgroup
+// tokens per prep workgroup when each thread takes TPT consecutive tokens
+constexpr int prep_tokens(int tpt) { return kPrepThreads / (kPrepChans / 8) * tpt; }
 constexpr int kConvTaps = 4;
 constexpr int kNormThreads = 256;
 
@@ -59,7 +60,7 @@ __device__ __forceinline__ int seq_of(const int32_t* __restrict__ cu, int n_seqs
 
 // One unit of k_la_prep: channel slab `slab` (or the gates when slab ==
 // chan_slabs) of token block `tb`.
-template <typename TP, typename TQ, int DK, int DV>
+template <typename TP, typename TQ, int DK, int DV, int TPT>
 __device__ __forceinline__ void prep_unit(int slab, int tb, int32_t T, int32_t n_seqs,
                                           const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                           const TP* __restrict__ P, int64_t ldp, int32_t chan0,
@@ -70,12 +71,12 @@ __device__ __forceinline__ void prep_unit(int slab, int tb, int32_t T, int32_t n
                                           float (*wlds)[kPrepChans]) {
   constexpr int H = kConvTaps - 1;
   const int cq = hk * DK, cv = hv * DV, nch = 2 * cq + cv;
-  const int t0 = tb * kPrepTokens;
+  const int t0 = tb * prep_tokens(TPT);
   const int tid = threadIdx.x;
 
   if (slab == chan_slabs) {   // gates
     const int ca = nch - chan0;
-    const int t1 = min(T, t0 + kPrepTokens);
+    const int t1 = min(T, t0 + prep_tokens(TPT));
     for (int i = tid; i < (t1 - t0) * hv; i += kPrepThreads) {
       const int t = t0 + i / hv, h = i % hv;
       const TP* row = P + static_cast<int64_t>(t) * ldp;
@@ -88,30 +89,37 @@ __device__ __forceinline__ void prep_unit(int slab, int tb, int32_t T, int32_t n
     return;
   }
 
-  const int t = t0 + tid / (kPrepChans / 8);
+  const int tt = t0 + TPT * (tid / (kPrepChans / 8));   // this thread's first token
   const int cg = tid % (kPrepChans / 8);
   const int c0 = chan0 + (slab * (kPrepChans / 8) + cg) * 8;
-  const bool active = c0 < nch && t < T;   // idle lanes still join the lane exchanges
+  const bool any = c0 < nch && tt < T;   // idle lanes still join the lane exchanges
   // Every global load of the unit is issued before anything waits: the
   // slab's conv taps (one coalesced 16-byte load per thread, channel
-  // slab * 256 + tid), the first token of this token's sequence, and the four
-  // rows t - 3 .. t (those before the sequence are zeroed afterwards).
+  // slab * 256 + tid) and the rows tt - 3 .. tt + TPT - 1 of this thread's
+  // eight channels, each loaded once for the TPT tokens that use it (rows
+  // before a token's sequence are zeroed afterwards).
   const int ch = chan0 + slab * kPrepChans + tid;
   const float4 w4 = ch < nch ? reinterpret_cast<const float4*>(conv_w)[ch] : make_float4(0.f, 0.f, 0.f, 0.f);
-  int first = 0;
-  float u[kConvTaps][8];
-  if (active) {
-    first = cu[seq_of(cu, n_seqs, t)];
+  float u[TPT + H][8];
+  int first[TPT];
+  if (any) {
     const TP* col = P + (c0 - chan0);
 #pragma unroll
-    for (int j = 0; j < kConvTaps; ++j) {
-      const int tj = t - H + j;
-      if (tj >= 0) {
-        load_run<TP, 8>(col + static_cast<int64_t>(tj) * ldp, u[j]);
+    for (int r = 0; r < TPT + H; ++r) {
+      const int tr = tt - H + r;
+      if (tr >= 0 && tr < T) {
+        load_run<TP, 8>(col + static_cast<int64_t>(tr) * ldp, u[r]);
       } else {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) u[j][e] = 0.0f;
+        for (int e = 0; e < 8; ++e) u[r][e] = 0.0f;
       }
+    }
+    // first token of each token's sequence (empty sequences skipped)
+    int sq = seq_of(cu, n_seqs, tt);
+#pragma unroll
+    for (int i = 0; i < TPT; ++i) {
+      while (sq + 1 < n_seqs && cu[sq + 1] <= tt + i) ++sq;
+      first[i] = cu[sq];
     }
   }
   // the taps, tap-major in LDS; each thread then reads its eight channels of
@@ -122,52 +130,60 @@ __device__ __forceinline__ void prep_unit(int slab, int tb, int32_t T, int32_t n
   wlds[2][tid] = w4.z;
   wlds[3][tid] = w4.w;
   lds_barrier();
-  float c[8];
+  float w[kConvTaps][8];
 #pragma unroll
-  for (int e = 0; e < 8; ++e) c[e] = 0.0f;
-  if (active) {
-    float w[kConvTaps][8];
+  for (int j = 0; j < kConvTaps; ++j) {
+    const f32x4 lo = *reinterpret_cast<const f32x4*>(&wlds[j][cg * 8]);
+    const f32x4 hi = *reinterpret_cast<const f32x4*>(&wlds[j][cg * 8 + 4]);
 #pragma unroll
-    for (int j = 0; j < kConvTaps; ++j) {
-      const f32x4 lo = *reinterpret_cast<const f32x4*>(&wlds[j][cg * 8]);
-      const f32x4 hi = *reinterpret_cast<const f32x4*>(&wlds[j][cg * 8 + 4]);
+    for (int e = 0; e < 4; ++e) { w[j][e] = lo[e]; w[j][4 + e] = hi[e]; }
+  }
+  const int sec = c0 < cq ? 0 : (c0 < 2 * cq ? 1 : 2);
 #pragma unroll
-      for (int e = 0; e < 4; ++e) { w[j][e] = lo[e]; w[j][4 + e] = hi[e]; }
-      if (t - H + j < first) {   // before the sequence: zero history
+  for (int i = 0; i < TPT; ++i) {
+    const int t = tt + i;
+    const bool active = any && t < T;
+    float c[8];
 #pragma unroll
-        for (int e = 0; e < 8; ++e) u[j][e] = 0.0f;
+    for (int e = 0; e < 8; ++e) c[e] = 0.0f;
+    if (active) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float acc = 0.0f;
+#pragma unroll
+        for (int j = 0; j < kConvTaps; ++j)   // before the sequence: zero history
+          acc += w[j][e] * (t - H + j >= first[i] ? u[i + j][e] : 0.0f);
+        c[e] = silu_f(acc);
       }
     }
+    float ss = 0.0f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      c[e] = silu_f(w[0][e] * u[0][e] + w[1][e] * u[1][e] + w[2][e] * u[2][e] + w[3][e] * u[3][e]);
+    for (int e = 0; e < 8; ++e) ss += c[e] * c[e];
+    // sum of squares over the head (DK / 8 lanes); used by q and k lanes only
+#pragma unroll
+    for (int off = 1; off < DK / 8; off <<= 1) ss += __shfl_xor(ss, off, kWave);
+    if (!active) continue;
+    if (sec < 2) {
+      const float r = rsqrtf(ss + l2_eps);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) c[e] *= r;
+    }
+    TQ* dst;
+    if (sec == 0) dst = q + static_cast<int64_t>(t) * cq + c0;
+    else if (sec == 1) dst = k + static_cast<int64_t>(t) * cq + (c0 - cq);
+    else dst = v + static_cast<int64_t>(t) * cv + (c0 - 2 * cq);
+    store8(dst, c);
   }
-  float ss = 0.0f;
-#pragma unroll
-  for (int e = 0; e < 8; ++e) ss += c[e] * c[e];
-  // sum of squares over the head (DK / 8 lanes); used by q and k lanes only
-#pragma unroll
-  for (int off = 1; off < DK / 8; off <<= 1) ss += __shfl_xor(ss, off, kWave);
-  if (!active) return;
-  const int sec = c0 < cq ? 0 : (c0 < 2 * cq ? 1 : 2);
-  if (sec < 2) {
-    const float r = rsqrtf(ss + l2_eps);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) c[e] *= r;
-  }
-  TQ* dst;
-  if (sec == 0) dst = q + static_cast<int64_t>(t) * cq + c0;
-  else if (sec == 1) dst = k + static_cast<int64_t>(t) * cq + (c0 - cq);
-  else dst = v + static_cast<int64_t>(t) * cv + (c0 - 2 * cq);
-  store8(dst, c);
 }
 
 // P [T, ldp] (TP) holds the in-projection from channel chan0 on: q|k|v
 // channels chan0 .. 2 cq + cv, then a [hv], then b [hv].  chan0 = 0 computes
 // q, k and v; chan0 = cq (no queries) k and v only.
-// One thread per (token, eight channels): a workgroup covers kPrepTokens
-// tokens x kPrepChans channels, thread (tok, cg) = (tid / 32, tid % 32), and
-// loads the four rows its taps need (the neighbours' rows come from L1).
+// One thread per (TPT consecutive tokens, eight channels): a workgroup covers
+// prep_tokens(TPT) tokens x kPrepChans channels, thread (tok, cg) = (tid / 32,
+// tid % 32), and loads each row its taps need once.  TPT = 4 when there are
+// enough tokens to keep every workgroup of the grid busy (fewer loads per
+// token, more of them in flight per thread), else 1 (more units, more waves).
 // Units: chan_slabs channel slabs plus one gate slab per token block; unit u
 // is xcd-remapped to logical index token_block * (chan_slabs + 1) + slab, so
 // an XCD streams whole rows of P, token after token.  The
@@ -175,7 +191,7 @@ __device__ __forceinline__ void prep_unit(int slab, int tb, int32_t T, int32_t n
 // units, so waves live long enough to keep many loads in flight: one short
 // wave per unit leaves the CUs mostly waiting for wave launches.  The stride
 // is a multiple of 8, so a unit runs on the XCD its remap assumes.
-template <typename TP, typename TQ, int DK, int DV>
+template <typename TP, typename TQ, int DK, int DV, int TPT>
 __global__ __launch_bounds__(kPrepThreads)
 void k_la_prep(int32_t T, int32_t n_seqs, const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                const TP* __restrict__ P, int64_t ldp, int32_t chan0, int32_t chan_slabs,
@@ -188,7 +204,7 @@ void k_la_prep(int32_t T, int32_t n_seqs, const int32_t* __restrict__ cu, int32_
   for (int unit = blockIdx.x; unit < total; unit += gridDim.x) {   // uniform per workgroup
     const int logical = xcd_remap(unit, total);
     const int slabs = chan_slabs + 1;
-    prep_unit<TP, TQ, DK, DV>(logical % slabs, logical / slabs, T, n_seqs, cu, hk, hv, P,
+    prep_unit<TP, TQ, DK, DV, TPT>(logical % slabs, logical / slabs, T, n_seqs, cu, hk, hv, P,
                               ldp, chan0, chan_slabs, conv_w, a_log, dt_bias, l2_eps, q, k, v, g, beta,
                               wlds);
   }

@@ -23,7 +23,8 @@
 namespace gdn {
 namespace {
 
-static_assert(kPrepTokens == kBlockPrepTokens && kPrepChans == kBlockPrepChans && kConvTaps == kBlockConvTaps,
+static_assert(prep_tokens(1) == kBlockPrepTokensPerThreadRow && kPrepChans == kBlockPrepChans &&
+                  kConvTaps == kBlockConvTaps,
               "host and device tiling agree");
 
 constexpr int32_t kBlockStagesOut = 5;
@@ -53,7 +54,8 @@ void launch_prep(const BlockPlan& p, const gdn_la_shape& s, const gdn_la_weights
                  char* ws, hipStream_t stream) {
   const uint32_t blocks = static_cast<uint32_t>(p.prep_grid);
   TA* q = p.outputs ? reinterpret_cast<TA*>(ws + p.off_q) : nullptr;
-  hipLaunchKernelGGL((k_la_prep<TA, TA, DK, DV>), dim3(blocks), dim3(kPrepThreads), 0, stream,
+  auto kernel = p.prep_tpt == 4 ? k_la_prep<TA, TA, DK, DV, 4> : k_la_prep<TA, TA, DK, DV, 1>;
+  hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kPrepThreads), 0, stream,
                      static_cast<int32_t>(p.T), s.num_seqs, cu, s.num_k_heads, s.num_v_heads,
                      reinterpret_cast<const TA*>(ws + p.off_P), p.ldp,
                      static_cast<int32_t>(p.outputs ? 0 : p.cq), static_cast<int32_t>(p.prep_slabs - 1),

@@ -97,7 +97,8 @@ inline int64_t split_groups(const gdn_shape& s) {
 // Workspace the two projections may use (hipBLASLt's split-k kernels).
 constexpr size_t kGemmWorkspace = size_t{32} << 20;
 constexpr int kBlockConvTaps = 4;
-constexpr int kBlockPrepTokens = 8;   // tokens per prep workgroup (kPrepTokens on the device)
+// tokens per prep workgroup: 8 x (tokens per thread, 1 or 4: prep_tokens on the device)
+constexpr int kBlockPrepTokensPerThreadRow = 8;
 constexpr int kBlockPrepChans = 256;  // channels per prep workgroup (kPrepChans)
 // Grid cap of the two elementwise kernels: 8 workgroups of 256 threads per CU
 // of the 256-CU MI355X (a multiple of 8, one per XCD); they stride over the rest.
@@ -117,6 +118,7 @@ struct BlockPlan {
   size_t act_bytes = 0;
   size_t off_P = 0, off_q = 0, off_k = 0, off_v = 0, off_g = 0, off_beta = 0, off_o = 0;
   size_t off_scan = 0, off_gemm = 0, bytes = 0;
+  int32_t prep_tpt = 1;                            // tokens per prep thread (1 or 4)
   int64_t prep_token_blocks = 0, prep_slabs = 0;   // channel slabs, plus one gate slab
   int64_t prep_grid = 0;                            // workgroups launched (<= units)
   int64_t norm_blocks = 0, norm_grid = 0;

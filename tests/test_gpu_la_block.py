@@ -134,6 +134,19 @@ def test_block_parity_layer_shape(act, outputs):
     _check("layer shape, tail 819", x, cu, w, dims, 128 ** -0.5, outputs, act)
 
 
+@pytest.mark.parametrize("act", ["f32", "bf16"])
+@pytest.mark.parametrize("outputs", [True, False])
+def test_block_prep_four_tokens_per_thread(act, outputs):
+    """Enough tokens that the prep kernel takes four consecutive tokens per
+    thread (one-token units would fill its grid four times over): sequences
+    of 1, 2 and 3 tokens put sequence starts inside a thread's four tokens."""
+    dims = LayerDims(hidden=256, hk=2, hv=4, dk=128, dv=128)
+    lens = [6001, 1, 2, 3, 5, 7000, 130]
+    assert sum(lens) // 8 * 5 >= 4 * 2048   # 5 prep slabs at this shape
+    x, cu, w = _case(207, dims, lens)
+    _check("four tokens per prep thread", x, cu, w, dims, 0.1, outputs, act)
+
+
 def test_block_parity_several_tails_layer_shape():
     dims = LayerDims(hidden=2048, hk=16, hv=32, dk=128, dv=128)
     x, cu, w = _case(202, dims, [410, 64, 129, 7])
