@@ -250,3 +250,56 @@ def test_split_replay_agrees_with_one_chain(r, slow):
     print(f"[split] r={r}: split vs one chain {e:.2e}, fused tail vs one chain {e_mid:.2e}", flush=True)
     assert e <= 1e-5
     assert torch.equal(mid, chain[:1])
+
+
+def test_varlen_graph_with_longest_first_order():
+    """An unsorted varlen batch whose scan grids exceed the chip (64-wide tail
+    scan, whole-head forward): both run in longest-first order, which travels
+    in the kernels' arguments.  Tail replay and forward captured in one HIP
+    graph replay bitwise like the eager calls, three times, with other eager
+    work between the replays."""
+    shape = synth.Shape(hk=8, hv=16, dk=128, dv=128, dtype="bf16")
+    lens = [70, 700, 3, 300, 1000, 64]          # 6 x 16 x 4 = 384 column groups > 256 CUs
+    p = synth.pack([_seq(i, n, shape=shape) for i, n in enumerate(lens)])
+    x = device_inputs(p)
+    n = len(lens)
+    st = torch.empty((n, shape.hv, shape.dk, shape.dv), dtype=torch.float32, device="cuda")
+    st2 = torch.empty_like(st)
+    o = torch.empty_like(x["v"])
+    ws_t = torch.empty(gdn.workspace_size(n, shape.hk, shape.hv, shape.dk, shape.dv, p.cu_seqlens.tolist()) + 256,
+                       dtype=torch.uint8, device="cuda")
+    ws_f = torch.empty(gdn.workspace_size(n, shape.hk, shape.hv, shape.dk, shape.dv, p.cu_seqlens.tolist(),
+                                          with_outputs=True) + 256, dtype=torch.uint8, device="cuda")
+
+    def calls():
+        gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"], state_out=st, workspace=ws_t)
+        gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"], state_in=st,
+                          o=o, state_out=st2, workspace=ws_f, scale=0.5)
+
+    calls()
+    torch.cuda.synchronize()
+    ref = (st.clone(), st2.clone(), o.clone())
+    # each sequence as its own call: the order only moves work between workgroups
+    for i, s in enumerate(lens):
+        xi = device_inputs(synth.pack([_seq(i, s, shape=shape)]))
+        sti = gdn.tail_replay(xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"], xi["cu_host"])
+        assert state_err(to_f64(ref[0][i:i + 1]), to_f64(sti)) <= 1e-5
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        calls()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        calls()
+    for rep in range(3):
+        st.zero_()
+        st2.zero_()
+        o.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(st, ref[0]) and torch.equal(st2, ref[1]) and torch.equal(o, ref[2]), f"replay {rep}"
+        junk = torch.randn(1 << 20, device="cuda").sum()
+        torch.cuda.synchronize()
+        del junk
