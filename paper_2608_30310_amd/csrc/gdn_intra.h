@@ -64,10 +64,12 @@ struct IntraLds {
   static constexpr int AP = kChunk + 4;             // fp32 row pitch of A, T and P
   // The per-wave block scratch of the off-diagonal inverse steps takes the
   // keys' place: the last key reads (the K record) end before those steps.
-  // Without it the tail-replay variant (bf16, d_k = 128) needs 57.6 KiB and
-  // two workgroups fit on a CU; with it 53.3 KiB, and three fit.
   // Likewise P takes the queries' place: it stays in registers until the Q
-  // record is written (the forward variant: 87.5 -> 70 KiB, two per CU).
+  // record is written.  And T = (I + A)^-1 is formed in A's place: every
+  // step of the inversion reads the blocks of A it needs before it writes the
+  // T block that replaces one of them, and never reads that A block again.
+  // Sizes (bf16, d_k = 128): tail replay 36 KiB, forward 53 KiB, three
+  // workgroups per CU either way (the register budget allows three).
   union {
     alignas(16) uint16_t Ks[NL][kChunk][KP];
     alignas(16) float Ys[4][16][17];
@@ -76,8 +78,7 @@ struct IntraLds {
     alignas(16) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
     alignas(16) float Ps[FWD ? kChunk : 1][AP];
   };
-  alignas(16) float As[kChunk][AP];                 // A (strictly lower)
-  alignas(16) float Ts[kChunk][AP];                 // T = (I + A)^-1
+  alignas(16) float As[kChunk][AP];                 // A (strictly lower), then T = (I + A)^-1
   alignas(16) float Gs[kChunk];
   alignas(16) float Bs[kChunk];
   static_assert(sizeof(float[4][16][17]) <= sizeof(uint16_t[NL][kChunk][KP]), "block scratch fits in the keys");
@@ -108,7 +109,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   auto& Ks = sm.Ks;
   auto& Qs = sm.Qs;
   auto& As = sm.As;
-  auto& Ts = sm.Ts;
+  auto& Ts = sm.As;   // T overwrites A block by block (see IntraLds)
   auto& Ps = sm.Ps;
   auto& Ys = sm.Ys;
   auto& Gs = sm.Gs;
