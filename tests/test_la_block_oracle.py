@@ -8,6 +8,9 @@ independently of it (CPU only).
     scale beta v (k . q) of the block's own q, k, v (the recurrence receives
     the right columns), with alpha = beta = 1/2 when the gate inputs vanish
     (softplus(0) = ln 2, sigmoid(0) = 1/2);
+  * gate parameters away from zero (A_log = (ln 2, ln 3), dt_bias = (1, -1/2),
+    zero gate inputs) give g = -exp(A_log) softplus(dt_bias) in closed form
+    per head, and two tokens carry that gate into the state as Eq. 1 says;
   * q and k come out with unit norm; g <= 0 and 0 < beta < 1;
   * the gated RMS norm removes any positive scale of o (o is linear in V
     from the zero state), with a worked case of exact decimals;
@@ -83,6 +86,32 @@ def pin_single_token(block):
         kk, qq, vv = p["k"][0, h * HK // HV], p["q"][0, h * HK // HV], p["v"][0, h]
         np.testing.assert_allclose(state[0, h], 0.5 * np.outer(kk, vv), rtol=1e-12, atol=1e-15)
         np.testing.assert_allclose(p["o"][0, h], 0.5 * 0.5 * vv * (kk @ qq), rtol=1e-12, atol=1e-15)
+
+
+def pin_gate_closed_form(block):
+    """Gate parameters away from zero: with the a and b rows of W_in zeroed,
+    a = b = 0, so beta = 1/2 and g[h] = -exp(A_log[h]) softplus(dt_bias[h])
+    exactly.  A_log = (ln 2, ln 3) and dt_bias = (1, -1/2) give
+    g = (-2 ln(1 + e), -3 ln(1 + e^{-1/2})).  Two tokens carry the gate into
+    the state: M2 = alpha2 (M1 - beta2 k2 (k2^T M1)) + beta2 k2 v2^T with
+    M1 = beta1 k1 v1^T, alpha2 = exp(g[h]) (Eq. 1, transposed layout)."""
+    rng = np.random.default_rng(11)
+    w = _weights(rng)
+    cq, cv = HK * DK, HV * DV
+    w["w_in"][2 * cq + cv:2 * cq + cv + 2 * HV] = 0.0
+    w["a_log"] = np.array([np.log(2.0), np.log(3.0)])
+    w["dt_bias"] = np.array([1.0, -0.5])
+    want_g = np.array([-2.0 * np.log1p(np.e), -3.0 * np.log1p(np.exp(-0.5))])
+    x = rng.standard_normal((2, D))
+    state, _, p = _run(x, w, np.array([0, 2]), block)
+    np.testing.assert_allclose(p["g"], np.broadcast_to(want_g, (2, HV)), rtol=1e-14)
+    np.testing.assert_allclose(p["beta"], 0.5, rtol=1e-14)
+    for h in range(HV):
+        k1, k2 = p["k"][0, h * HK // HV], p["k"][1, h * HK // HV]
+        v1, v2 = p["v"][0, h], p["v"][1, h]
+        m1 = 0.5 * np.outer(k1, v1)
+        m2 = np.exp(want_g[h]) * (m1 - 0.5 * np.outer(k2, k2 @ m1)) + 0.5 * np.outer(k2, v2)
+        np.testing.assert_allclose(state[0, h], m2, rtol=1e-12, atol=1e-15)
 
 
 def pin_norms_and_gate_ranges(block):
@@ -190,7 +219,8 @@ def pin_what_depends_on_what(block):
     np.testing.assert_allclose(s2, s0, rtol=1e-13, atol=1e-15)
 
 
-BLOCK_PINS = [pin_what_depends_on_what, pin_single_token, pin_norms_and_gate_ranges, pin_gated_norm,
+BLOCK_PINS = [pin_what_depends_on_what, pin_single_token, pin_gate_closed_form, pin_norms_and_gate_ranges,
+              pin_gated_norm,
               pin_out_is_linear_in_w_out, pin_zero_prefix_changes_nothing,
               pin_zero_gate_silences_output]
 
@@ -266,6 +296,19 @@ MUTANTS = {
     "silu as identity": ("block", _block_with(silu=lambda x: x)),
     "norm without the rms": ("block", _block_with(gated_rmsnorm=lambda o, z, w, e: o * w * lb.silu(z))),
     "l2 norm missing": ("block", _block_with(l2norm=lambda x, e: x)),
+    "gate without exp(A_log)": ("block", _block_with(
+        gates=lambda a, b, al, dt: (-lb.softplus(a + np.asarray(dt)[None, :]), lb.sigmoid(b)))),
+    "gate with A_log not exponentiated": ("block", _block_with(
+        gates=lambda a, b, al, dt: (-np.asarray(al)[None, :] * lb.softplus(a + np.asarray(dt)[None, :]),
+                                    lb.sigmoid(b)))),
+    "gate with a - dt_bias": ("block", _block_with(
+        gates=lambda a, b, al, dt: (-np.exp(np.asarray(al))[None, :] * lb.softplus(a - np.asarray(dt)[None, :]),
+                                    lb.sigmoid(b)))),
+    "gate with exp(-A_log)": ("block", _block_with(
+        gates=lambda a, b, al, dt: (-np.exp(-np.asarray(al))[None, :] * lb.softplus(a + np.asarray(dt)[None, :]),
+                                    lb.sigmoid(b)))),
+    "gate parameters of the wrong head": ("block", _block_with(
+        gates=lambda a, b, al, dt, _g=lb.gates: _g(a, b, np.asarray(al)[::-1], np.asarray(dt)[::-1]))),
     "a and b swapped": ("block", _rows_read_as("qkvbaz")),
     "q and k swapped": ("block", _rows_read_as("kqvabz")),
 }
