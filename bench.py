@@ -4,26 +4,27 @@
 One step = the whole hot path over one batch of resident synthetic input:
 Independent Tail-Replay of every value head's state from zero over the last
 r tokens of the matched prefix (paper Section 3, Eq. 2), then the chunked
-forward over the new suffix from the rebuilt states, emitting its outputs.
+forward over the new suffix from the rebuilt state, emitting its outputs.
 
-Default workload: one GDN layer with hybrid-model head shapes (16 key heads,
-32 value heads, d_k = d_v = 128, bf16 q/k/v, fp32 g/beta/state), matched
-prefix 8192 tokens, replay tail 819 tokens (10 %), 512 suffix tokens.
+Default workload: a stack of 36 GDN layers with hybrid-model head shapes
+(16 key heads, 32 value heads, d_k = d_v = 128, bf16 q/k/v, fp32 g/beta/state),
+each with its own seeded inputs; matched prefix 32768 tokens, replay tail 3277
+tokens (10 %), 1024 new suffix tokens.  The step runs the layers one after the
+other, as the layers of a group depend on each other (paper Section 3): per
+layer ``gdn_tail_replay`` then ``gdn_chunk_forward`` from the rebuilt state,
+launched eagerly on one stream.  ``value`` = tokens through the path per
+second, 36 x (3277 + 1024) per step.  Beside it: the same step replayed from a
+HIP graph, the 36 layers as one batched call (layers as sequences), the
+rebuild latency of the 36 replays (warm, cold, queued), per-stage kernel
+durations from HIP events that the library records on the stream its kernels
+run on, ``roofline`` for the dominant kernel, the one-layer workload
+(tail 819 + suffix 512) and ``cpu_baseline`` (the fp64 oracle on the same
+inputs on the host cores).
 
-Prints ONE JSON line.  ``value`` is tokens through the path per second
-(tail + suffix tokens per step / step time): the step is one
-``gdn_replay_forward`` call (replay, then the suffix forward from the rebuilt
-state, the suffix's chunk preparation overlapped with the tail's scan),
-launched eagerly on one stream.  ``ms_per_step_two_calls`` times the same work
-as ``gdn_tail_replay`` + ``gdn_chunk_forward``, ``ms_per_step_graph`` the fused
-step replayed from a HIP graph.  Per-stage kernel durations come from HIP
-events that the library records between its kernels on the stream the kernels
-run on, in a separate pass of the same steps; ``roofline`` describes the
-dominant kernel.
-
-``--summarize-pmc FETCH_DIR WRITE_DIR`` (no GPU) turns two rocprofv3 --pmc
-runs of ``bench.py --calib-copy`` (FETCH_SIZE, then WRITE_SIZE) into the
-traffic summary under profiles/ that later runs report as ``traffic``.
+``--sweep`` times the other workloads (one JSON line each); ``--summarize-pmc
+FETCH_DIR WRITE_DIR`` (no GPU) turns two rocprofv3 --pmc runs of ``bench.py
+--calib-copy`` (FETCH_SIZE, then WRITE_SIZE) into the traffic summary under
+profiles/ that later runs report as ``traffic``.
 """
 from __future__ import annotations
 
@@ -46,7 +47,7 @@ CHUNK = 64
 CALIB_BYTES = 1 << 30          # plain copy used to calibrate the PMC byte counters (> the 256 MB MALL)
 FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
 QUEUE_SPIN_CYCLES = 2_000_000  # spin kernel (~0.8 ms) that outlasts the host's enqueue of one call
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload1_r{r}.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload2.json")
 KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
                   "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
                   "paper_2608_30310_amd/csrc/gdn_intra.h", "paper_2608_30310_amd/csrc/gdn_scan.h",
@@ -59,14 +60,17 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--replay", type=int, default=819, choices=[410, 819],
-                    help="replay tail length of the 8192-token prefix")
+    ap.add_argument("--layers", type=int, default=36,
+                    help="layers of the stack (the workload has 36; fewer only for quick checks)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
-                    help="approximate CPU time for the oracle baseline sample")
+                    help="approximate wall time of each oracle baseline sample (all cores, one thread)")
+    ap.add_argument("--procs", type=int, default=0,
+                    help="threads drawing the seeded inputs (default: usable cores, at most 16)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
-    ap.add_argument("--cold-reps", type=int, default=20,
-                    help="tail replays timed after an Infinity Cache flush")
+    ap.add_argument("--no-workload1", action="store_true", help="skip the one-layer workload's extra keys")
+    ap.add_argument("--cold-reps", type=int, default=10,
+                    help="rebuilds of the stack timed after an Infinity Cache flush")
     ap.add_argument("--calib-copy", action="store_true",
                     help="also run plain device copies of a known size (PMC calibration)")
     ap.add_argument("--summarize-pmc", nargs=2, metavar=("FETCH_DIR", "WRITE_DIR"))
@@ -76,11 +80,11 @@ def parse():
                     help="with --summarize-pmc: workload description stored in the summary")
     ap.add_argument("--sweep", action="store_true",
                     help="time the other workloads instead (one JSON line each): small fp32 layer, "
-                         "36-layer stack, 16 varlen hits, decode steps, FA-KV transfer overlap, layer-block replay, "
-                         "replay-vs-full at 8K/16K/32K")
+                         "one layer at tail 410, full prefill vs tails with the error bound, 16 varlen hits, "
+                         "decode steps, FA-KV transfer overlap, layer-block replay, replay-vs-full at 8K/16K/32K")
     ap.add_argument("--only", default="",
                     help="with --sweep: comma list of sections to run "
-                         "(small, layer410, stack, hits, decode, h2d, block, full)")
+                         "(small, layer410, accuracy, hits, decode, h2d, block, full)")
     ap.add_argument("--decode-seqs", default="1,64,256",
                     help="with --sweep: batch sizes of the decode lines")
     return ap.parse_args()
@@ -161,7 +165,7 @@ def _calibration(rows, counter):
     return key[0], statistics.fmean(cands[key])
 
 
-def summarize_pmc(fetch_dir, write_dir, replay, out_path=None, workload=None):
+def summarize_pmc(fetch_dir, write_dir, out_path=None, workload=None):
     frows, wrows = _counter_rows(fetch_dir), _counter_rows(write_dir)
     fetch = _per_kernel_mean(frows, "FETCH_SIZE")
     write = _per_kernel_mean(wrows, "WRITE_SIZE")
@@ -172,14 +176,14 @@ def summarize_pmc(fetch_dir, write_dir, replay, out_path=None, workload=None):
     f_write = CALIB_BYTES / (cal_write * 1024.0)
     kernels = {}
     for name in fetch:
-        if not any(t in name for t in ("k_scan", "k_intra", "k_decode")):
+        if not any(t in name for t in ("k_scan", "k_intra", "k_decode", "k_state_combine")):
             continue
         short = name.split("(")[0].replace("void ", "")
         fb = fetch[name] * 1024.0 * f_fetch
         wb = write.get(name, 0.0) * 1024.0 * f_write
         kernels[short] = {"fetch_kib": fetch[name], "write_kib": write.get(name, 0.0),
                           "fetch_bytes": fb, "write_bytes": wb, "traffic_bytes": fb + wb}
-    summary = {"workload": workload or f"one layer Hk=16 Hv=32 d=128 bf16, tail {replay} + suffix 512",
+    summary = {"workload": workload or WORKLOAD2_NAME,
                "source_sha256": kernel_source_hash(),
                "calibration": {"kernel": cname.split("(")[0], "bytes_each_way": CALIB_BYTES,
                                "fetch_kib": cal_fetch, "write_kib": cal_write,
@@ -188,20 +192,20 @@ def summarize_pmc(fetch_dir, write_dir, replay, out_path=None, workload=None):
                "commands": [
                    "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE "
                    "--output-format csv -d $OUT/pmc_fetch -o fetch -- python3 $ROOT/bench.py "
-                   "--no-cpu-baseline --no-graph --steps 5 --warmup 2 --cold-reps 0 --calib-copy",
+                   "--no-cpu-baseline --no-graph --no-workload1 --steps 5 --warmup 2 --cold-reps 0 --calib-copy",
                    "(same with WRITE_SIZE into $OUT/pmc_write)",
                    f"python bench.py --summarize-pmc $OUT/pmc_fetch $OUT/pmc_write"]}
-    path = out_path or TRAFFIC_FILE.format(r=replay)
+    path = out_path or TRAFFIC_FILE
     with open(path, "w") as f:
         json.dump(summary, f, indent=1)
     print(json.dumps(summary, indent=1))
     return path
 
 
-def load_traffic(replay, kernel_short):
+def load_traffic(kernel_short):
     """Calibrated HBM bytes per launch of `kernel_short` from the committed PMC
     summary, or None when there is none or the kernels changed since."""
-    path = TRAFFIC_FILE.format(r=replay)
+    path = TRAFFIC_FILE
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -212,11 +216,34 @@ def load_traffic(replay, kernel_short):
     return None if k is None else k["traffic_bytes"]
 
 
+# ---------------------------------------------------------------- inputs
+WORKLOAD2_NAME = ("36-layer stack, one GDN layer each: Hk=16 Hv=32 d_k=d_v=128 bf16 q/k/v; prefix 32768, "
+                  "tail replay r=3277 from zero + 1024-token suffix forward with outputs, per layer")
+
+
+def usable_cores():
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
+
+
 # ---------------------------------------------------------------- main
 def main():
     args = parse()
     if args.summarize_pmc:
-        summarize_pmc(*args.summarize_pmc, args.replay, args.pmc_out, args.pmc_workload)
+        summarize_pmc(*args.summarize_pmc, args.pmc_out, args.pmc_workload)
         return
     if args.sweep:
         sweep(args)
@@ -228,11 +255,22 @@ def main():
         sys.exit(2)
 
     import numpy as np
+
+    import synth
+    from synth import workloads
+
+    # ---- seeded inputs (drawn on a pool of threads)
+    t_draw = time.perf_counter()
+    shape, hits = workloads.workload2(args.layers)
+    drawn = workloads.draw_hits(hits, shape, threads=args.procs)
+    tails = synth.pack([t for t, _ in drawn])
+    sufs = synth.pack([s for _, s in drawn])
+    del drawn
+    t_draw = time.perf_counter() - t_draw
+
     import torch
 
     import paper_2608_30310_amd as gdn
-    import synth
-    from synth import workloads
 
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
@@ -240,11 +278,6 @@ def main():
     gdn.load_library()
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-
-    shape, hits = workloads.workload1(args.replay)
-    hit = hits[0]
-    tail = synth.pack([hit.tail(shape)])
-    suf = synth.pack([hit.suffix(shape)])
 
     def to_dev(p):
         def qkv(a):
@@ -254,22 +287,117 @@ def main():
                     cu=torch.from_numpy(p.cu_seqlens).to(dev),
                     cu_host=torch.from_numpy(p.cu_seqlens.copy()))
 
-    xt, xs = to_dev(tail), to_dev(suf)
-    N, hk, hv, dk, dv = 1, shape.hk, shape.hv, shape.dk, shape.dv
-    state = torch.empty((N, hv, dk, dv), dtype=torch.float32, device=dev)
-    state2 = torch.empty_like(state)
-    o = torch.empty((suf.num_tokens, hv, dv), dtype=torch.bfloat16, device=dev)
-    ws_t = torch.empty(gdn.workspace_size(N, hk, hv, dk, dv, tail.cu_seqlens.tolist()) + 256,
+    xt, xs = to_dev(tails), to_dev(sufs)
+    L = args.layers
+    hk, hv, dk, dv = shape.hk, shape.hv, shape.dk, shape.dv
+    r, s = hits[0].r, hits[0].s
+    # per-layer views of the packed inputs: each layer is its own one-sequence call
+    cu_t1, cu_s1 = [0, r], [0, s]
+    cu_t1_d = torch.tensor(cu_t1, dtype=torch.int32, device=dev)
+    cu_s1_d = torch.tensor(cu_s1, dtype=torch.int32, device=dev)
+    cu_t1_h = torch.tensor(cu_t1, dtype=torch.int32)
+    cu_s1_h = torch.tensor(cu_s1, dtype=torch.int32)
+    lt = [{n: xt[n][l * r:(l + 1) * r] for n in ("k", "v", "g", "beta")} for l in range(L)]
+    ls = [{n: xs[n][l * s:(l + 1) * s] for n in ("q", "k", "v", "g", "beta")} for l in range(L)]
+    mid = torch.empty((L, hv, dk, dv), dtype=torch.float32, device=dev)
+    fin = torch.empty_like(mid)
+    o = torch.empty((L * s, hv, dv), dtype=torch.bfloat16, device=dev)
+    ws_t = torch.empty(gdn.workspace_size(1, hk, hv, dk, dv, cu_t1) + 256, dtype=torch.uint8, device=dev)
+    ws_f = torch.empty(gdn.workspace_size(1, hk, hv, dk, dv, cu_s1, with_outputs=True) + 256,
                        dtype=torch.uint8, device=dev)
-    ws_f = torch.empty(gdn.workspace_size(N, hk, hv, dk, dv, suf.cu_seqlens.tolist(),
-                                          with_outputs=True) + 256,
-                       dtype=torch.uint8, device=dev)
-    ws_rf = torch.empty(gdn.replay_forward_workspace_size(N, hk, hv, dk, dv, tail.cu_seqlens.tolist(),
-                                                          suf.cu_seqlens.tolist()) + 256,
+    names_t, names_f = gdn.stage_names(False), gdn.stage_names(True)
+
+    def replay_layer(l, ev=None):
+        x = lt[l]
+        gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], cu_t1_d, cu_t1_h, state_out=mid[l:l + 1],
+                        workspace=ws_t, events=ev)
+
+    def forward_layer(l, ev=None):
+        x = ls[l]
+        gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], cu_s1_d, cu_s1_h, state_in=mid[l:l + 1],
+                          o=o[l * s:(l + 1) * s], state_out=fin[l:l + 1], workspace=ws_f, events=ev)
+
+    def step(evs=None):
+        for l in range(L):
+            replay_layer(l, evs[l][0] if evs else None)
+            forward_layer(l, evs[l][1] if evs else None)
+
+    def rebuild():
+        for l in range(L):
+            replay_layer(l)
+
+    # the layers as one batched call each (layers as the sequences of one launch)
+    midb, finb = torch.empty_like(mid), torch.empty_like(fin)
+    ob = torch.empty_like(o)
+    ws_bt = torch.empty(gdn.workspace_size(L, hk, hv, dk, dv, tails.cu_seqlens.tolist()) + 256,
                         dtype=torch.uint8, device=dev)
-    names_t = gdn.stage_names(False)
-    names_f = gdn.stage_names(True)
-    names_rf = gdn.replay_forward_stage_names()
+    ws_bf = torch.empty(gdn.workspace_size(L, hk, hv, dk, dv, sufs.cu_seqlens.tolist(), with_outputs=True)
+                        + 256, dtype=torch.uint8, device=dev)
+
+    def batched_replay():
+        gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"], state_out=midb,
+                        workspace=ws_bt)
+
+    def batched_step():
+        batched_replay()
+        gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
+                          state_in=midb, o=ob, state_out=finb, workspace=ws_bf)
+
+    for _ in range(args.warmup):
+        step()
+        batched_step()
+    torch.cuda.synchronize()
+    K = args.steps
+
+    def timed(fn, reps=K):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        start.record()
+        for _ in range(reps):
+            fn()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / reps
+
+    # ---- graph of one step, checked bitwise against the eager step on several replays
+    graph, graph_note = None, None
+    step()
+    torch.cuda.synchronize()
+    want = (mid.clone(), fin.clone(), o.clone())
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            step()
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step()
+        ok = True
+        for _ in range(3):
+            for t in (mid, fin, o):
+                t.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            ok = ok and torch.equal(mid, want[0]) and torch.equal(fin, want[1]) and torch.equal(o, want[2])
+            step()               # eager work between replays
+            torch.cuda.synchronize()
+        if ok:
+            graph = g
+        else:
+            graph_note = "graph replay differed from the eager step; graph not timed"
+    # the batched form computes the same states up to rounding order
+    batched_step()
+    torch.cuda.synchronize()
+    bdiff = float(((finb - want[1]).norm() / want[1].norm()).item())
+
+    ms_per_step = timed(step)
+    ms_graph = timed(graph.replay) if graph is not None else None
+    ms_batched = timed(batched_step)
+    ms_batched_rebuild = timed(batched_replay)
+
+    # ---- per-stage kernel durations: events recorded by the library on its stream
+    n_ev = min(K, 20)
 
     def new_events(n):
         evs = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
@@ -277,95 +405,31 @@ def main():
             e.record()
         return evs
 
-    def replay_call(ev=None):
-        gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"],
-                        state_out=state, workspace=ws_t, events=ev)
-
-    def forward_call(ev=None):
-        gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
-                          state_in=state, o=o, state_out=state2, workspace=ws_f, events=ev)
-
-    def two_calls(ev_t=None, ev_f=None):
-        replay_call(ev_t)
-        forward_call(ev_f)
-
-    def step(ev=None):
-        gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xs["q"], xs["k"], xs["v"],
-                           xs["g"], xs["beta"], xs["cu"], cu_tail_host=xt["cu_host"],
-                           cu_suf_host=xs["cu_host"], state_mid=state, o=o, state_out=state2,
-                           workspace=ws_rf, events=ev)
-
-    for _ in range(args.warmup):
-        step()
-        two_calls()
+    evs = [[(new_events(len(names_t) + 1), new_events(len(names_f) + 1)) for _ in range(L)] for _ in range(n_ev)]
     torch.cuda.synchronize()
-    K = args.steps
-
-    def timed(fn):
-        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        start.record()
-        for _ in range(K):
-            fn()
-        stop.record()
-        torch.cuda.synchronize()
-        return start.elapsed_time(stop) / K
-
-    # ---- graph of one step, checked bitwise against the eager step on several replays
-    graph, graph_note = None, None
-    if not args.no_graph:
-        step()
-        torch.cuda.synchronize()
-        want_s, want_o = state2.clone(), o.clone()
-        g = torch.cuda.CUDAGraph()
-        with torch.cuda.graph(g):
-            step()
-        ok = True
-        for _ in range(3):
-            state2.zero_()
-            o.zero_()
-            g.replay()
-            torch.cuda.synchronize()
-            ok = ok and torch.equal(state2, want_s) and torch.equal(o, want_o)
-            step()               # eager work between replays
-            torch.cuda.synchronize()
-        if ok:
-            graph = g
-        else:
-            graph_note = "graph replay differed from the eager step; graph not timed"
-
-    ms_per_step = timed(step)
-    ms_two = timed(two_calls)
-    ms_graph = timed(graph.replay) if graph is not None else None
-
-    # ---- per-stage kernel durations: events recorded by the library on its stream
-    ev_rf = [new_events(len(names_rf) + 1) for _ in range(K)]
-    torch.cuda.synchronize()
-    for i in range(K):
-        step(ev_rf[i])
-    torch.cuda.synchronize()
-    ev_t = [new_events(len(names_t) + 1) for _ in range(K)]
-    ev_f = [new_events(len(names_f) + 1) for _ in range(K)]
-    torch.cuda.synchronize()
-    for i in range(K):
-        two_calls(ev_t[i], ev_f[i])
+    for i in range(n_ev):
+        step(evs[i])
     torch.cuda.synchronize()
     stages = {}
-    for prefix, names, evs in (("replay_forward", names_rf, ev_rf), ("tail_replay", names_t, ev_t),
-                               ("chunk_forward", names_f, ev_f)):
+    for part, names in ((0, names_t), (1, names_f)):
+        prefix = ("tail_replay.", "chunk_forward.")[part]
         for j, nm in enumerate(names):
-            d = [evs[i][j].elapsed_time(evs[i][j + 1]) * 1e3 for i in range(K)]
-            stages[f"{prefix}.{nm}"] = {"mean_us": statistics.fmean(d),
-                                        "median_us": statistics.median(d)}
-    warm = quantiles([ev_t[i][0].elapsed_time(ev_t[i][-1]) * 1e3 for i in range(K)])
+            d = [evs[i][l][part][j].elapsed_time(evs[i][l][part][j + 1]) * 1e3
+                 for i in range(n_ev) for l in range(L)]
+            stages[prefix + nm] = {"mean_us": statistics.fmean(d), "median_us": statistics.median(d),
+                                   "per_step_us": statistics.fmean(d) * L}
 
-    # ---- the same with the call's launches already queued: a spin kernel
-    # holds the GPU while the host enqueues the call, so the interval is the
-    # device's alone (kernels and the gaps between them, no host pacing)
-    def queued(fn):
+    # ---- rebuild latency of the stack (the 36 replays): warm (from an idle
+    #      stream), queued (a spin kernel holds the GPU while the host enqueues,
+    #      so the interval is the device's alone) and cold (Infinity Cache
+    #      flushed before each rep)
+    def latency(fn, reps, before=None, spin=False):
         lat = []
-        for _ in range(K):
-            torch.cuda._sleep(QUEUE_SPIN_CYCLES)
+        for i in range(reps):
+            if before:
+                before(i)
+            if spin:
+                torch.cuda._sleep(QUEUE_SPIN_CYCLES * max(1, L // 4))
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
             fn()
@@ -374,22 +438,12 @@ def main():
             lat.append(a.elapsed_time(b) * 1e3)
         return quantiles(lat)
 
-    queued_rebuild = queued(replay_call)
-
-    # ---- cold rebuild latency: Infinity Cache flushed before each tail replay
+    warm = latency(rebuild, min(K, 20))
+    queued_rebuild = latency(rebuild, min(K, 20), spin=True)
     cold = None
     if args.cold_reps > 0:
         flush = torch.empty(FLUSH_BYTES // 4, dtype=torch.float32, device=dev)
-        lat = []
-        for i in range(args.cold_reps):
-            flush.fill_(float(i))
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            replay_call()
-            b.record()
-            torch.cuda.synchronize()
-            lat.append(a.elapsed_time(b) * 1e3)
-        cold = quantiles(lat)
+        cold = latency(rebuild, args.cold_reps, before=lambda i: flush.fill_(float(i)))
         del flush
 
     if args.calib_copy:
@@ -401,44 +455,43 @@ def main():
         torch.cuda.synchronize()
         del src, dst
 
-    # ---- algorithmic work
+    # ---- algorithmic work (SURVEY-style per-token counts, full 64-token tiles)
     elt = 2
-    r, s = hit.r, hit.s
     ft, bt = per_token_work(hk, hv, dk, dv, elt, outputs=False)
     ff, bf = per_token_work(hk, hv, dk, dv, elt, outputs=True)
-    state_bytes = N * hv * dk * dv * 4
+    state_bytes = hv * dk * dv * 4          # one layer's states
     tail_flops, tail_bytes = r * hv * ft, r * hv * bt + state_bytes
     fwd_flops, fwd_bytes = s * hv * ff, s * hv * bf + 2 * state_bytes
-    path_flops, path_bytes = tail_flops + fwd_flops, tail_bytes + fwd_bytes
+    path_flops, path_bytes = L * (tail_flops + fwd_flops), L * (tail_bytes + fwd_bytes)
     t_s = ms_per_step * 1e-3
     path_bound_s = max(path_flops / (BF16_PEAK_TFLOPS * 1e12), path_bytes / (HBM_PEAK_GBS * 1e9))
 
-    # dominant kernel: the stage of the timed (fused) step with the largest
-    # mean time; its algorithmic bytes are those of the part of the path it
-    # runs (the tail replay's or the suffix forward's)
-    fused = {k: v for k, v in stages.items() if k.startswith("replay_forward.")}
-    dom = max(fused, key=lambda k: fused[k]["mean_us"])
+    # dominant kernel: the stage with the most time per step; its algorithmic
+    # bytes are those of the part of the path it runs, per launch (one layer)
+    dom = max(stages, key=lambda k: stages[k]["per_step_us"])
     grp = hv // hk
-    # the suffix's chunk preparation reads q, k (shared by the group), g and
-    # beta and forms K K^T and Q K^T per chunk
-    prep_bytes = s * hv * (2 * elt * dk / grp + 8)
-    prep_flops = s * hv * (2 * 2 * CHUNK * dk / grp)
-    kbytes, kflops = {"replay_forward.tail intra": (tail_bytes, tail_flops),
-                      "replay_forward.tail scan + suffix intra": (tail_bytes + prep_bytes,
-                                                                  tail_flops + prep_flops),
-                      "replay_forward.suffix scan": (fwd_bytes, fwd_flops)}[dom]
+    split = stages["tail_replay.combine"]["mean_us"] > 0.5
+    kinfo = {
+        "tail_replay.intra": ("gdn::k_intra<unsigned short, 128, false>",
+                              r * hv * (elt * dk / grp + 8), r * hv * 2 * CHUNK * dk / grp),
+        "tail_replay.scan": ("gdn::k_scan_cols_split<unsigned short, 128>" if split
+                             else "gdn::k_scan_cols<unsigned short, 128, false>", tail_bytes, tail_flops),
+        "tail_replay.combine": ("gdn::k_state_combine<128>", 3 * state_bytes + hv * dk * dk * 4,
+                                2 * hv * dk * dk * dv),
+        "chunk_forward.intra": ("gdn::k_intra<unsigned short, 128, true>",
+                                s * hv * (2 * elt * dk / grp + 8), s * hv * 2 * 2 * CHUNK * dk / grp),
+        "chunk_forward.scan": ("gdn::k_scan_cols<unsigned short, 128, true>", fwd_bytes, fwd_flops),
+    }
+    kname, kbytes, kflops = kinfo[dom]
     dom_s = stages[dom]["mean_us"] * 1e-6
     achieved = kbytes / dom_s / 1e9
-    kname = {"replay_forward.tail intra": "gdn::k_intra<unsigned short, 128, false>",
-             "replay_forward.tail scan + suffix intra": "gdn::k_scan_cols_intra<unsigned short, 128>",
-             "replay_forward.suffix scan": "gdn::k_scan_cols<unsigned short, 128, true>"}.get(dom)
-    traffic = load_traffic(args.replay, kname) if kname else None
-    roofline = {"kernel": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": traffic,
-                "algorithmic_bytes_per_launch": kbytes,
+    roofline = {"kernel": kname, "stage": dom, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": load_traffic(kname.split("(")[0]),
+                "algorithmic_bytes_per_launch": kbytes, "algorithmic_flops_per_launch": kflops,
+                "launch_us": stages[dom]["mean_us"],
                 "mfma_frac": kflops / dom_s / (BF16_PEAK_TFLOPS * 1e12)}
 
-    tokens = r + s
+    tokens = L * (r + s)
     result = {
         "metric": METRIC,
         "value": tokens / t_s,
@@ -451,33 +504,107 @@ def main():
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
-        "data": "synthetic",
-        "config": {"workload": f"one GDN layer, Hk=16 Hv=32 d_k=d_v=128 bf16 q/k/v; "
-                               f"prefix 8192, tail replay r={r} from zero + {s}-token suffix "
-                               f"forward with outputs",
-                   "global_batch": 1, "seq_len": r + s, "parallelism": "single GPU"},
-        "launch": "eager, gdn_replay_forward",
-        "ms_per_step_two_calls": ms_two,
+        "data": "synthetic (seeded per 64-token block; see synth/)",
+        "config": {"workload": WORKLOAD2_NAME if L == 36 else f"{L}-layer stack (reduced), shapes as the "
+                                                              f"36-layer workload",
+                   "layers": L, "prefix": hits[0].m, "tail": r, "suffix": s,
+                   "global_batch": L, "seq_len": r + s, "parallelism": "single GPU"},
+        "launch": "eager; per layer gdn_tail_replay then gdn_chunk_forward, layers in sequence",
         "ms_per_step_graph": ms_graph,
+        "ms_per_step_batched": ms_batched,
+        "batched_vs_sequential_rel_state_diff": bdiff,
         "rebuild_latency_us": warm["p50"],
         "rebuild_latency_warm_us": warm,
         "rebuild_latency_cold_us": cold,
         "rebuild_latency_queued_us": queued_rebuild,
-        "replay_tokens_per_s": r / (warm["p50"] * 1e-6),
+        "rebuild_latency_batched_us": ms_batched_rebuild * 1e3,
+        "replay_tokens_per_s": L * r / (warm["p50"] * 1e-6),
+        "replay_tokens_per_s_batched": L * r / (ms_batched_rebuild * 1e-3),
         "stages": stages,
         "path": {"flops": path_flops, "bytes": path_bytes, "roofline_us": path_bound_s * 1e6,
                  "roofline_frac": path_bound_s / t_s,
                  "mfma_frac": path_flops / t_s / (BF16_PEAK_TFLOPS * 1e12)},
         "roofline": roofline,
         "cpu_baseline": None,
+        "input_draw_s": t_draw,
         "gpu": torch.cuda.get_device_name(dev),
     }
     if graph_note:
         result["note"] = graph_note
-
+    if not args.no_workload1:
+        result["workload1"] = workload1_line(args, gdn, torch, dev)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(tail, suf, r, s, args.cpu_seconds)
+        result["cpu_baseline"] = cpu_baseline(tails, sufs, r, s, args.cpu_seconds)
     print(json.dumps(result), flush=True)
+
+
+def workload1_line(args, gdn, torch, dev):
+    """The one-layer workload (tail 819 + suffix 512) as extra keys: the fused
+    call, the two calls, and the rebuild latency."""
+    import numpy as np
+
+    import synth
+    from synth import workloads
+    shape, hits = workloads.workload1(819)
+    h = hits[0]
+    tail, suf = synth.pack([h.tail(shape)]), synth.pack([h.suffix(shape)])
+
+    def to_dev(p):
+        qkv = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)
+        return dict(q=qkv(p.q), k=qkv(p.k), v=qkv(p.v), g=torch.from_numpy(p.g).to(dev),
+                    beta=torch.from_numpy(p.beta).to(dev), cu=torch.from_numpy(p.cu_seqlens).to(dev),
+                    cu_host=torch.from_numpy(p.cu_seqlens.copy()))
+
+    xt, xs = to_dev(tail), to_dev(suf)
+    hv, dk, dv = shape.hv, shape.dk, shape.dv
+    st = torch.empty((1, hv, dk, dv), dtype=torch.float32, device=dev)
+    st2 = torch.empty_like(st)
+    o = torch.empty((h.s, hv, dv), dtype=torch.bfloat16, device=dev)
+
+    def fused():
+        gdn.replay_forward(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xs["q"], xs["k"], xs["v"],
+                           xs["g"], xs["beta"], xs["cu"], cu_tail_host=xt["cu_host"],
+                           cu_suf_host=xs["cu_host"], state_mid=st, o=o, state_out=st2)
+
+    def replay():
+        gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"], state_out=st)
+
+    def two():
+        replay()
+        gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
+                          state_in=st, o=o, state_out=st2)
+
+    for _ in range(5):
+        fused()
+        two()
+    torch.cuda.synchronize()
+
+    def timed(fn, reps=args.steps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    def lat(fn, reps=20):
+        xs_ = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            xs_.append(a.elapsed_time(b) * 1e3)
+        return quantiles(xs_)
+
+    ms_fused = timed(fused)
+    return {"workload": "one GDN layer Hk=16 Hv=32 d=128 bf16: prefix 8192, tail 819 + suffix 512",
+            "ms_per_step_fused": ms_fused, "ms_per_step_two_calls": timed(two),
+            "tokens_per_s_fused": (h.r + h.s) / (ms_fused * 1e-3),
+            "rebuild_latency_us": lat(replay)}
 
 
 # ---------------------------------------------------------------- other workloads
@@ -492,6 +619,7 @@ def sweep(args):
 
     import paper_2608_30310_amd as gdn
     import synth
+    from paper_2608_30310_amd import transfer
     from synth import workloads
 
     dev = torch.device("cuda:0")
@@ -575,6 +703,47 @@ def sweep(args):
 
     want = lambda name: not args.only or name in args.only.split(",")
 
+    def oracle_time(tail, suf, seconds=args.cpu_seconds):
+        """The fp64 oracle on the host cores on a workload's own inputs: the
+        tail replay then the suffix forward from its state, all heads, on every
+        usable core; then on one thread over the value heads of the first key
+        head only (bounded wall time).  Rates in (token, value head) pairs per
+        second, so the two are comparable; the all-core run also as tokens/s."""
+        import oracle
+
+        def run(p_t, p_s, threads):
+            n, t0 = 0, time.perf_counter()
+            while True:
+                et, es = p_t.exact(), p_s.exact()
+                _, st = oracle.recurrence(et["k"], et["v"], et["g"], et["beta"], et["cu_seqlens"], nthreads=threads)
+                if p_s.num_tokens:
+                    oracle.recurrence(es["k"], es["v"], es["g"], es["beta"], es["cu_seqlens"], q=es["q"],
+                                      state_in=st, nthreads=threads)
+                n += 1
+                el = time.perf_counter() - t0
+                if el >= seconds / 2 or n >= 50:
+                    return n, el
+
+        def first_group(p):
+            import dataclasses
+            grp = p.shape.hv // p.shape.hk
+            shp = dataclasses.replace(p.shape, hk=1, hv=grp)
+            return synth.Packed(shp, p.q[:, :1].copy(), p.k[:, :1].copy(), p.v[:, :grp].copy(),
+                                p.g[:, :grp].copy(), p.beta[:, :grp].copy(), p.cu_seqlens)
+
+        tokens = tail.num_tokens + suf.num_tokens
+        cores = min(usable_cores(), oracle.max_threads())
+        n_all, el_all = run(tail, suf, cores)
+        t1, s1 = first_group(tail), first_group(suf)
+        n_one, el_one = run(t1, s1, 1)
+        return {"kind": "oracle", "cpu_model": cpu_model(),
+                "all_cores": {"cores": cores, "tokens_per_s": n_all * tokens / el_all,
+                              "head_tokens_per_s": n_all * tokens * tail.shape.hv / el_all,
+                              "sample": f"{n_all} run(s) of every head in {el_all:.2f} s"},
+                "one_thread": {"cores": 1, "head_tokens_per_s": n_one * tokens * t1.shape.hv / el_one,
+                               "sample": f"{n_one} run(s) of the {t1.shape.hv} value heads of key head 0 "
+                                         f"in {el_one:.2f} s"}}
+
     # ---- small fp32 layer (Hk = Hv = 4, d = 64): tail 205 + suffix 256
     if want("small"):
         shape, hits = workloads.workload0()
@@ -590,7 +759,8 @@ def sweep(args):
         emit({"workload": "small fp32 layer Hk=Hv=4 d=64: tail 205 + suffix 256",
               "rebuild_latency_us": rep, "rebuild_latency_queued_us": repq,
               "step_us": both, "step_two_calls_us": two,
-              "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6)})
+              "tokens_per_s": (205 + 256) / (both["p50"] * 1e-6),
+              "cpu_oracle": oracle_time(synth.pack([h.tail(shape)]), synth.pack([h.suffix(shape)]))})
 
     # ---- hybrid-model layer, tail 410 (the default bench line covers 819)
     if want("layer410"):
@@ -609,20 +779,57 @@ def sweep(args):
               "step_us": both, "step_two_calls_us": two,
               "tokens_per_s": (410 + 512) / (both["p50"] * 1e-6)})
 
-    # ---- 36-layer stack, m = 32768, r = 3277: 36 sequential per-layer replays,
-    #      and the batched variant (layers as 36 sequences of one launch)
-    if want("stack"):
-        L, r2 = 36, 3277
-        xl = [random_dev([r2], 16, 32, 128, seed=100 + l) for l in range(L)]
-        wsl, stl, _ = buffers(xl[0], 1, 16, 32, 128, False)
-        seq = timed_us(lambda: [replay(x, stl, wsl) for x in xl])
-        xb = random_dev([r2] * L, 16, 32, 128, seed=7)
-        wsb, stb, _ = buffers(xb, L, 16, 32, 128, False)
-        bat = timed_us(lambda: replay(xb, stb, wsb))
-        emit({"workload": "36-layer stack Hk=16 Hv=32 d=128 bf16, m=32768, tail 3277 per layer",
-              "rebuild_latency_sequential_us": seq, "rebuild_latency_batched_us": bat,
-              "replay_tokens_per_s_sequential": L * r2 / (seq["p50"] * 1e-6),
-              "replay_tokens_per_s_batched": L * r2 / (bat["p50"] * 1e-6)})
+    # ---- full prefill against tail replay, one layer, m = 32768 (seeded
+    #      inputs of that workload): for every replay length r and gate scale,
+    #      the tail state's relative distance from the full-prefill state next
+    #      to the bound ||S_head||_F prod(alpha) / ||S_full||_F (S_head = the
+    #      full-prefill state at m - r; prod(alpha) = exp(sum of g over the
+    #      tail)), maxima over the 32 value heads, log10 of the bound, and the
+    #      time ratio of the full forward (with outputs) to the tail replay; plus
+    #      the fp64 oracle's time on the full prefix (all cores; one thread over
+    #      the two value heads of key head 0)
+    if want("accuracy"):
+        for gs in workloads.WORKLOAD4_GATE_SCALES:
+            shape, hit = workloads.workload4(3277, gs)
+            full = synth.pack([hit.prefix(shape)])
+            xf = packed_dev(full, shape)
+            wsF, stF, oF = buffers(xf, 1, 16, 32, 128, True)
+            t_full = timed_us(lambda: forward(xf, None, oF, stF, wsF), queued=True)
+            s_full = stF.double().cpu().numpy()[0]
+            g_all = full.g.astype(np.float64)
+            cells = []
+            for r in workloads.WORKLOAD4_TAILS:
+                m = hit.m
+                # the tail's inputs are rows [m - r, m) of the full prefix
+                xt = {n: xf[n][m - r:] for n in ("k", "v", "g", "beta")}
+                xt["cu"] = torch.tensor([0, r], dtype=torch.int32, device=dev)
+                xt["cu_host"] = torch.tensor([0, r], dtype=torch.int32)
+                xh = {n: xf[n][:m - r] for n in ("k", "v", "g", "beta")}
+                xh["cu"] = torch.tensor([0, m - r], dtype=torch.int32, device=dev)
+                xh["cu_host"] = torch.tensor([0, m - r], dtype=torch.int32)
+                wst, st, _ = buffers(xt, 1, 16, 32, 128, False)
+                wsh, sth, _ = buffers(xh, 1, 16, 32, 128, False)
+                t_rep = timed_us(lambda: replay(xt, st, wst), queued=True)
+                replay(xh, sth, wsh)
+                torch.cuda.synchronize()
+                s_tail = st.double().cpu().numpy()[0]
+                s_head = sth.double().cpu().numpy()[0]
+                log_prod = g_all[m - r:].sum(axis=0) / np.log(10.0)       # per head, log10 prod(alpha)
+                n_full = np.linalg.norm(s_full.reshape(32, -1), axis=1)
+                rel = np.linalg.norm((s_full - s_tail).reshape(32, -1), axis=1) / n_full
+                n_head = np.linalg.norm(s_head.reshape(32, -1), axis=1)
+                with np.errstate(divide="ignore"):
+                    log_bound = np.log10(n_head / n_full) + log_prod
+                cells.append({"r": r, "rel_err_max": float(rel.max()), "rel_err_median": float(np.median(rel)),
+                              "log10_bound_max": float(log_bound.max()),
+                              "log10_prod_alpha_mean": float(log_prod.mean()),
+                              "bound_holds_all_heads": bool(np.all(rel <= 10.0 ** log_bound + 4e-3)),
+                              "t_replay_us": t_rep["p50"], "time_ratio_full_over_replay": t_full["p50"] / t_rep["p50"]})
+            emit({"workload": f"full 32768-token prefill vs tail replay, one layer Hk=16 Hv=32 d=128 bf16, "
+                              f"gate scale {gs}",
+                  "t_full_forward_us": t_full["p50"], "cells": cells,
+                  "cpu_oracle_full_prefix": oracle_time(full, synth.pack([], shape))})
+            del xf, oF
 
     # ---- 16 concurrent hits (varlen), one replay launch + one forward launch
     if want("hits"):
@@ -644,7 +851,9 @@ def sweep(args):
               "rebuild_latency_us": rep, "rebuild_latency_queued_us": repq,
               "step_us": both, "step_two_calls_us": two,
               "tokens_per_s": (sr + ss) / (both["p50"] * 1e-6),
-              "replay_tokens_per_s": sr / (rep["p50"] * 1e-6)})
+              "replay_tokens_per_s": sr / (rep["p50"] * 1e-6),
+              "cpu_oracle": oracle_time(synth.pack([h.tail(shape) for h in hits]),
+                                        synth.pack([h.suffix(shape) for h in hits]))})
 
     # ---- decode steps after the rebuild: one token per sequence from the state,
     #      state updated in place; HBM-bound (the state is read and written once,
@@ -712,25 +921,16 @@ def sweep(args):
                 for x in xq:
                     forward(x, st, o, st2, wsf)
 
-            def h2d(stream):
-                with torch.cuda.stream(stream):
-                    dev_kv.copy_(host_kv, non_blocking=True)
-
-            main = torch.cuda.current_stream()
+            def h2d():
+                dev_kv.copy_(host_kv, non_blocking=True)
 
             def serial():
-                h2d(main)
-                replays()
-                forwards()
+                transfer.rebuild_serial(host_kv, dev_kv, replays, forwards)
 
             def overlapped():
-                copy_stream.wait_stream(main)
-                h2d(copy_stream)
-                replays()
-                main.wait_stream(copy_stream)
-                forwards()
+                transfer.rebuild_overlapped(host_kv, dev_kv, replays, forwards, copy_stream)
 
-            t_h2d = timed_us(lambda: h2d(main))
+            t_h2d = timed_us(h2d)
             t_rep = timed_us(replays)
             t_fwd = timed_us(forwards)
             t_ser = timed_us(serial)
@@ -848,26 +1048,48 @@ def sweep(args):
                       "speedup_state_only_full": t_state["p50"] / t_rep["p50"]})
 
 
-def cpu_baseline(tail, suf, r, s, seconds):
-    """The fp64 oracle, as it stands, on the host cores: the same step repeated
-    until about ``seconds`` of CPU time have passed."""
+def _layer(p, l):
+    """Sequence l of a packed batch as its own one-sequence batch."""
+    import synth
+    a, b = int(p.cu_seqlens[l]), int(p.cu_seqlens[l + 1])
+    import numpy as np
+    return synth.Packed(p.shape, p.q[a:b], p.k[a:b], p.v[a:b], p.g[a:b], p.beta[a:b],
+                        np.array([0, b - a], np.int32))
+
+
+def cpu_baseline(tails, sufs, r, s, seconds):
+    """The fp64 oracle, as it stands, on the host cores, on the same seeded
+    inputs as the GPU step: layer after layer (the tail replay from zero, then
+    the suffix forward from the replayed state, all 32 heads), until about
+    ``seconds`` of wall time have passed; once on every usable core and once on
+    one thread.  ``value`` is the all-core rate."""
     import oracle
-    ext, exs = tail.exact(), suf.exact()
-    threads = oracle.max_threads()
-    reps = 0
-    t0 = time.perf_counter()
-    while True:
-        _, st = oracle.recurrence(ext["k"], ext["v"], ext["g"], ext["beta"], ext["cu_seqlens"])
-        oracle.recurrence(exs["k"], exs["v"], exs["g"], exs["beta"], exs["cu_seqlens"],
-                          q=exs["q"], state_in=st)
-        reps += 1
-        el = time.perf_counter() - t0
-        if el >= seconds or reps >= 200:
-            break
-    return {"value": reps * (r + s) / el, "unit": "tokens/s", "cores": threads,
-            "kind": "oracle",
-            "sample": f"{reps} steps of the default workload (all 32 heads, tail {r} + suffix {s}) "
-                      f"in {el:.2f} s wall on {threads} threads ({platform.processor() or 'cpu'})"}
+
+    def run(threads):
+        layers = 0
+        t0 = time.perf_counter()
+        while True:
+            t, f = _layer(tails, layers % tails.num_seqs), _layer(sufs, layers % sufs.num_seqs)
+            et, ef = t.exact(), f.exact()
+            _, st = oracle.recurrence(et["k"], et["v"], et["g"], et["beta"], et["cu_seqlens"], nthreads=threads)
+            oracle.recurrence(ef["k"], ef["v"], ef["g"], ef["beta"], ef["cu_seqlens"], q=ef["q"], state_in=st,
+                              nthreads=threads)
+            layers += 1
+            el = time.perf_counter() - t0
+            if el >= seconds or layers >= tails.num_seqs:
+                return layers, el
+
+    cores = min(usable_cores(), oracle.max_threads())
+    n_all, el_all = run(cores)
+    n_one, el_one = run(1)
+    model = cpu_model()
+    return {"value": n_all * (r + s) / el_all, "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "sample": f"{n_all} of the stack's layers (tail {r} from zero + suffix {s} with outputs, all 32 "
+                      f"heads, the bench's own seeded inputs) in {el_all:.2f} s wall on {cores} threads, {model}; "
+                      f"fp64 token-by-token recurrence, OpenMP over (sequence, value head)",
+            "cpu_model": model,
+            "single_thread": {"value": n_one * (r + s) / el_one, "unit": "tokens/s", "cores": 1,
+                              "sample": f"{n_one} layer(s) in {el_one:.2f} s wall on 1 thread"}}
 
 
 if __name__ == "__main__":

@@ -155,7 +155,9 @@ gdn_status gdn_chunk_forward_profiled(const gdn_shape* shape,
                                       void* stream,
                                       void* const* stage_events, int32_t num_events);
 
-/* Number of kernel stages a call enqueues, and the name of stage i. */
+/* Number of kernel stages a call enqueues, and the name of stage i:
+ * tail replay (with_outputs = 0) "intra", "scan", "combine" (the last is empty
+ * unless the chain runs in two halves); forward "intra", "scan". */
 int32_t gdn_num_stages(int32_t with_outputs);
 const char* gdn_stage_name(int32_t with_outputs, int32_t stage);
 

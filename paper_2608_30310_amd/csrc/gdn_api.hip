@@ -63,11 +63,14 @@ struct Args {
   float* state_out;
   char* ws;
   hipStream_t stream;
-  void* const* events;   // NULL, or kNumStages + 1 hipEvent_t to record between stages
+  void* const* events;   // NULL, or num_stages(fwd) + 1 hipEvent_t to record between stages
 };
 
-constexpr int32_t kNumStages = 2;
-const char* const kStageNames[kNumStages] = {"intra", "scan"};
+// Stages of a call: tail replay {intra, scan, combine} (combine is empty
+// unless the chain runs in two halves), forward {intra, scan}.
+constexpr int32_t kMaxStages = 3;
+constexpr int32_t num_stages(bool fwd) { return fwd ? 2 : 3; }
+const char* const kStageNames[kMaxStages] = {"intra", "scan", "combine"};
 
 gdn_status mark(const Args& a, int stage) {
   if (!a.events) return GDN_OK;
@@ -77,8 +80,8 @@ gdn_status mark(const Args& a, int stage) {
   return GDN_OK;
 }
 
-gdn_status mark_all(const Args& a) {
-  for (int i = 0; i <= kNumStages; ++i) {
+gdn_status mark_all(const Args& a, bool fwd) {
+  for (int i = 0; i <= num_stages(fwd); ++i) {
     const gdn_status st = mark(a, i);
     if (st != GDN_OK) return st;
   }
@@ -115,9 +118,12 @@ gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups, int* c
   return GDN_OK;
 }
 
+// `marks` (tail replay only, may be NULL): the call whose stage events are
+// recorded; its combine stage starts before k_state_combine.
 template <typename TIn, int DK, int DV, bool FWD>
 gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, const void* v,
-                       const float* state_in, void* o, float* state_out, char* ws, hipStream_t stream) {
+                       const float* state_in, void* o, float* state_out, char* ws, hipStream_t stream,
+                       const Args* marks = nullptr, bool* combined = nullptr) {
   const u32x4* Kw = reinterpret_cast<const u32x4*>(ws + p.off_K);
   const u32x4* Tw = reinterpret_cast<const u32x4*>(ws + p.off_T);
   const float* Sw = reinterpret_cast<const float*>(ws + p.off_S);
@@ -138,6 +144,8 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
                          s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw,
                          state_out, m2, a2);
       if ((st = check_launch("split scan launch")) != GDN_OK) return st;
+      if (marks && (st = mark(*marks, 2)) != GDN_OK) return st;
+      if (combined) *combined = true;
       hipLaunchKernelGGL((k_state_combine<DK>),
                          dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCombineCols)),
                          dim3(kCombineThreads), 0, stream, s.d_v, a2, m2, state_out);
@@ -170,10 +178,15 @@ gdn_status run(const Args& a) {
   if ((st = launch_intra<TIn, DK, FWD>(s, *a.p, a.cu, a.q, a.k, a.g, a.beta, a.ws, a.stream)) != GDN_OK)
     return st;
   if ((st = mark(a, 1)) != GDN_OK) return st;
-  if ((st = launch_scan<TIn, DK, DV, FWD>(s, *a.p, a.cu, a.v, a.state_in, a.o, a.state_out, a.ws, a.stream)) !=
-      GDN_OK)
+  bool combined = false;
+  if ((st = launch_scan<TIn, DK, DV, FWD>(s, *a.p, a.cu, a.v, a.state_in, a.o, a.state_out, a.ws, a.stream,
+                                          FWD ? nullptr : &a, &combined)) != GDN_OK)
     return st;
-  return mark(a, 2);
+  if (!FWD && !combined) {
+    // one chain: the combine stage is empty
+    if ((st = mark(a, 2)) != GDN_OK) return st;
+  }
+  return mark(a, num_stages(FWD));
 }
 
 template <int DK, int DV, bool FWD>
@@ -224,9 +237,9 @@ gdn_status gdn_workspace_size(const gdn_shape* shape, const int32_t* cu_seqlens_
 namespace gdn {
 namespace {
 
-gdn_status check_events(void* const* events, int32_t num_events) {
+gdn_status check_events(void* const* events, int32_t num_events, bool fwd) {
   if (!events) return fail(GDN_ERR_NULL_ARG, "stage_events is NULL");
-  if (num_events != kNumStages + 1)
+  if (num_events != num_stages(fwd) + 1)
     return fail(GDN_ERR_BAD_SHAPE, "num_events must be gdn_num_stages() + 1");
   for (int i = 0; i < num_events; ++i)
     if (!events[i]) return fail(GDN_ERR_NULL_ARG, "a stage event is NULL");
@@ -250,7 +263,7 @@ gdn_status tail_replay_impl(const gdn_shape* shape, const int32_t* cu_seqlens_ho
   const gdn::Args a{shape, &plan, cu_seqlens, nullptr, k, v, g, beta, nullptr,
                     nullptr, state_out, static_cast<char*>(workspace),
                     static_cast<hipStream_t>(stream), events};
-  if (shape->num_seqs == 0) return mark_all(a);
+  if (shape->num_seqs == 0) return mark_all(a, false);
   return gdn::dispatch<false>(a);
 }
 
@@ -282,7 +295,7 @@ gdn_status chunk_forward_impl(const gdn_shape* shape, const int32_t* cu_seqlens_
   const gdn::Args a{shape, &plan, cu_seqlens, q, k, v, g, beta, state_in,
                     o, state_out, static_cast<char*>(workspace),
                     static_cast<hipStream_t>(stream), events};
-  if (shape->num_seqs == 0) return mark_all(a);
+  if (shape->num_seqs == 0) return mark_all(a, true);
   return gdn::dispatch<true>(a);
 }
 
@@ -491,7 +504,7 @@ gdn_status gdn_tail_replay_profiled(const gdn_shape* shape, const int32_t* cu_se
                                     const float* g, const float* beta, float* state_out,
                                     void* workspace, size_t workspace_bytes, void* stream,
                                     void* const* stage_events, int32_t num_events) {
-  const gdn_status st = gdn::check_events(stage_events, num_events);
+  const gdn_status st = gdn::check_events(stage_events, num_events, false);
   if (st != GDN_OK) return st;
   return gdn::tail_replay_impl(shape, cu_seqlens_host, cu_seqlens, k, v, g, beta, state_out,
                                workspace, workspace_bytes, stream, stage_events);
@@ -513,7 +526,7 @@ gdn_status gdn_chunk_forward_profiled(const gdn_shape* shape, const int32_t* cu_
                                       const float* state_in, void* o, float* state_out,
                                       void* workspace, size_t workspace_bytes, void* stream,
                                       void* const* stage_events, int32_t num_events) {
-  const gdn_status st = gdn::check_events(stage_events, num_events);
+  const gdn_status st = gdn::check_events(stage_events, num_events, true);
   if (st != GDN_OK) return st;
   return gdn::chunk_forward_impl(shape, cu_seqlens_host, cu_seqlens, q, k, v, g, beta,
                                  state_in, o, state_out, workspace, workspace_bytes, stream,
@@ -569,14 +582,10 @@ const char* gdn_replay_forward_stage_name(int32_t stage) {
   return gdn::kFusedStageNames[stage];
 }
 
-int32_t gdn_num_stages(int32_t with_outputs) {
-  (void)with_outputs;
-  return gdn::kNumStages;
-}
+int32_t gdn_num_stages(int32_t with_outputs) { return gdn::num_stages(with_outputs != 0); }
 
 const char* gdn_stage_name(int32_t with_outputs, int32_t stage) {
-  (void)with_outputs;
-  if (stage < 0 || stage >= gdn::kNumStages) return "";
+  if (stage < 0 || stage >= gdn::num_stages(with_outputs != 0)) return "";
   return gdn::kStageNames[stage];
 }
 

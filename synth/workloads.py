@@ -21,9 +21,11 @@ the paper's ceiling rule; this module only draws the ratio.
 """
 from __future__ import annotations
 
+import os
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
 from fractions import Fraction
-from typing import List, Tuple
+from typing import List, Sequence, Tuple
 
 import numpy as np
 
@@ -97,3 +99,24 @@ WORKLOAD4_GATE_SCALES = (0.02, 0.1, 0.5)
 
 def workload4(r: int, gate_scale: float) -> Tuple[Shape, Hit]:
     return HYBRID, Hit(4, 0, 0, 32768, r, 0, gate_scale)
+
+
+def draw_hits(hits: Sequence[Hit], shape: Shape, parts: Sequence[str] = ("tail", "suffix"),
+              threads: int = 0) -> List[Tuple[Tokens, ...]]:
+    """The named parts ("tail", "suffix", "prefix") of every hit, drawn on a
+    pool of threads (NumPy's generators and array kernels release the GIL).
+    The values are those of calling the parts one by one."""
+    if threads <= 0:
+        try:
+            threads = len(os.sched_getaffinity(0))
+        except AttributeError:
+            threads = os.cpu_count() or 1
+        threads = min(16, threads)
+
+    def one(h):
+        return tuple(getattr(h, p)(shape) for p in parts)
+
+    if threads == 1 or len(hits) <= 1:
+        return [one(h) for h in hits]
+    with ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(one, hits))

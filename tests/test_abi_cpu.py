@@ -238,6 +238,9 @@ def test_replay_forward_workspace_is_both_plans():
     assert st == 0 and out.value == (nt + 255) // 256 * 256 + ns
     assert gdn.replay_forward_workspace_size(2, 16, 32, 128, 128, ct, cs) == out.value
     assert gdn.replay_forward_stage_names() == ["tail intra", "tail scan + suffix intra", "suffix scan"]
+    assert gdn.stage_names(False) == ["intra", "scan", "combine"]
+    assert gdn.stage_names(True) == ["intra", "scan"]
+    assert lib.gdn_stage_name(0, 3) == b"" and lib.gdn_stage_name(1, 2) == b""
     # sequence counts must agree
     st = lib.gdn_replay_forward_workspace_size(ctypes.byref(_shape(num_seqs=2)),
                                                ctypes.cast(_cu(ct), ctypes.c_void_p),

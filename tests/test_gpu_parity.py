@@ -194,24 +194,74 @@ def _head_slice(p, h, grp):
 
 
 def test_workload2_layer_stack_sampled():
+    """The 36-layer stack (prefix 32768, tail 3277, suffix 1024) in both launch
+    forms the benchmark times: per layer, the tail replay (split in two
+    halves at this length) then the suffix forward from the rebuilt state; and
+    the 36 layers as one batched tail replay (the 64-wide column scan, 36 x 52
+    chunks in one launch) then one batched suffix forward (the whole-head
+    scan).  Sampled (layer, value head) units against the oracle: the rebuilt
+    state, the suffix outputs and the final state."""
     shape, hits = workloads.workload2()
     grp = shape.hv // shape.hk
-    sample_layers = {0, 17, 35}
+    sample_layers = [0, 17, 35]
     sample_heads = [0, 13, 31]
-    worst = 0.0
-    for hit in hits:                       # one launch per layer, as benchmarked
-        p = synth.pack([hit.tail(shape)])
-        x = device_inputs(p)
-        st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
-        if hit.layer not in sample_layers:
-            continue
-        got = to_f64(st)
+    drawn = workloads.draw_hits(hits, shape)
+    tails = synth.pack([t for t, _ in drawn])
+    sufs = synth.pack([s for _, s in drawn])
+    xt, xs = device_inputs(tails), device_inputs(sufs)
+    r, s = hits[0].r, hits[0].s
+    L = len(hits)
+    # per layer, as benchmarked
+    cu_t = torch.tensor([0, r], dtype=torch.int32)
+    cu_s = torch.tensor([0, s], dtype=torch.int32)
+    mid = torch.empty((L, shape.hv, 128, 128), dtype=torch.float32, device="cuda:0")
+    fin = torch.empty_like(mid)
+    o = torch.empty((L * s, shape.hv, 128), dtype=torch.bfloat16, device="cuda:0")
+    for l in range(L):
+        a, b = l * r, (l + 1) * r
+        gdn.tail_replay(xt["k"][a:b], xt["v"][a:b], xt["g"][a:b], xt["beta"][a:b], cu_t.cuda(), cu_t,
+                        state_out=mid[l:l + 1])
+        a, b = l * s, (l + 1) * s
+        gdn.chunk_forward(xs["q"][a:b], xs["k"][a:b], xs["v"][a:b], xs["g"][a:b], xs["beta"][a:b], cu_s.cuda(),
+                          cu_s, state_in=mid[l:l + 1], o=o[a:b], state_out=fin[l:l + 1])
+    # batched
+    midb = gdn.tail_replay(xt["k"], xt["v"], xt["g"], xt["beta"], xt["cu"], xt["cu_host"])
+    ob, finb = gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
+                                 state_in=midb)
+    torch.cuda.synchronize()
+    got = {name: to_f64(t) for name, t in (("mid", mid), ("fin", fin), ("o", o), ("midb", midb),
+                                            ("finb", finb), ("ob", ob))}
+    worst = dict(mid=0.0, fin=0.0, out=0.0, midb=0.0, finb=0.0, outb=0.0)
+    for l in sample_layers:
+        tp, sp = synth.pack([drawn[l][0]]), synth.pack([drawn[l][1]])
         for h in sample_heads:
-            k, v, g, b, cu, _ = _head_slice(p, h, grp)
-            _, want = oracle.recurrence(k, v, g, b, cu)
-            worst = max(worst, state_err(got[:, h:h + 1], want))
-    _report("workload2 36 layers r=3277 (sampled)", tail=worst)
-    assert worst <= STATE_TOL
+            k, v, g, b, cu, _ = _head_slice(tp, h, grp)
+            _, w_mid = oracle.recurrence(k, v, g, b, cu)
+            k2, v2, g2, b2, cu2, q2 = _head_slice(sp, h, grp)
+            w_o, w_fin = oracle.recurrence(k2, v2, g2, b2, cu2, q=q2, state_in=w_mid)
+            rows = slice(l * s, (l + 1) * s)
+            for tag in ("", "b"):
+                worst["mid" + tag] = max(worst["mid" + tag], state_err(got["mid" + tag][l:l + 1, h:h + 1], w_mid))
+                worst["fin" + tag] = max(worst["fin" + tag], state_err(got["fin" + tag][l:l + 1, h:h + 1], w_fin))
+                worst["out" + tag] = max(worst["out" + tag],
+                                         output_err(got["o" + tag][rows, h:h + 1], w_o, cu2))
+    _report("workload2 36 layers r=3277 s=1024 (sampled)", **worst)
+    assert max(worst["mid"], worst["fin"], worst["midb"], worst["finb"]) <= STATE_TOL
+    assert max(worst["out"], worst["outb"]) <= OUTPUT_TOL
+
+
+def _bound_check(st_full, st_tail, st_head, g_tail, slack):
+    """Per value head: ||S_full - S_tail||_F <= ||S_head||_F prod(alpha) + slack
+    ||S_full||_F, prod(alpha) = exp(sum of g over the tail) (the attenuation
+    bound of the replay).  Returns (max relative distance, max relative bound,
+    heads where it fails)."""
+    hv = st_full.shape[1]
+    full = st_full[0].reshape(hv, -1)
+    dist = np.linalg.norm(full - st_tail[0].reshape(hv, -1), axis=1)
+    nf = np.linalg.norm(full, axis=1)
+    bound = np.linalg.norm(st_head[0].reshape(hv, -1), axis=1) * np.exp(g_tail.sum(axis=0))
+    bad = [h for h in range(hv) if dist[h] > bound[h] + slack * nf[h]]
+    return float((dist / nf).max()), float((bound / nf).max()), bad
 
 
 @pytest.mark.parametrize("gate_scale", workloads.WORKLOAD4_GATE_SCALES)
@@ -232,6 +282,8 @@ def test_workload4_full_prefill_and_tails_sampled(gate_scale):
         got_o = to_f64(o[:, h:h + 1])
         e_o = max(e_o, output_err(got_o, w_o, cu))
     e_tail = 0.0
+    m = hit.m
+    bound_rows = []
     for r in workloads.WORKLOAD4_TAILS:
         _, hr = workloads.workload4(r, gate_scale)
         tp = synth.pack([hr.tail(shape)])
@@ -242,6 +294,18 @@ def test_workload4_full_prefill_and_tails_sampled(gate_scale):
             k, v, g, b, cu, _ = _head_slice(tp, h, grp)
             _, want = oracle.recurrence(k, v, g, b, cu)
             e_tail = max(e_tail, state_err(st[:, h:h + 1], want))
+        # the replay's attenuation bound on the GPU results, every value head:
+        # S_head is the full-prefill state at m - r (the head of the prefix,
+        # replayed from zero); slack for the two states' parity errors
+        cu_h = torch.tensor([0, m - r], dtype=torch.int32)
+        st_head = to_f64(gdn.tail_replay(x["k"][:m - r], x["v"][:m - r], x["g"][:m - r], x["beta"][:m - r],
+                                         cu_h.cuda(), cu_h))
+        rel, rel_bound, bad = _bound_check(got_st, st, st_head, full.g[m - r:].astype(np.float64), 2 * STATE_TOL)
+        bound_rows.append((r, rel, rel_bound))
+        assert not bad, f"bound fails at r={r} for heads {bad}"
+    print(f"[bound] gate scale {gate_scale}: " + "; ".join(
+        f"r={r}: |S_full-S_tail|/|S_full| max {rel:.2e} <= bound max {rb:.2e}" for r, rel, rb in bound_rows),
+        flush=True)
     _report(f"workload4 s={gate_scale} full 32K + tails (sampled)", full_state=e_st,
             full_out=e_o, tails=e_tail)
     assert e_st <= STATE_TOL and e_o <= OUTPUT_TOL and e_tail <= STATE_TOL

@@ -83,3 +83,14 @@ def test_layer_hiddens_tail_is_a_slice_and_weights_are_fixed():
     assert np.all((dt > 0.99e-3) & (dt < 1.01e-1))
     x, cu = pack_hiddens([hiddens(5, 0, i, 0, n, 64) for i, n in enumerate([3, 0, 70])], 64)
     assert list(cu) == [0, 3, 3, 73] and x.shape == (73, 64)
+
+
+def test_threaded_draw_equals_one_by_one():
+    shape = synth.Shape(2, 4, 16, 8, "bf16")
+    hits = [workloads.Hit(9, l, 0, 300, 70, 40) for l in range(5)]
+    got = workloads.draw_hits(hits, shape, threads=4)
+    for h, (t, s) in zip(hits, got):
+        want_t, want_s = h.tail(shape), h.suffix(shape)
+        for name in ("q", "k", "v", "g", "beta"):
+            assert np.array_equal(getattr(t, name), getattr(want_t, name))
+            assert np.array_equal(getattr(s, name), getattr(want_s, name))
