@@ -15,8 +15,10 @@ multiplied in the passes a variant names:
     qm   Q M0        "2": Q (hi + lo)(M0)           "1": Q hi(M0)
     pd   P Delta     "3", "2a", "2b", "1" as for T R (P in the place of T)
 Results are rounded to fp32 where the kernels hold fp32 (R, Delta, M1) and
-outputs to the storage dtype (``out_bf16``).
-The kernels' own choice is km=2, tr=3, ktd=2, qm=2, pd=3.
+outputs to the storage dtype (``out_bf16``).  The model covers bf16 inputs (K
+and Q exact operands).  The kernels' choice for bf16 inputs is ``KERNEL``:
+km=2, tr=2a, ktd=2, qm=2, pd=3 (``ALL_PASSES`` is the three-pass form they
+used before).
 """
 from __future__ import annotations
 
@@ -38,7 +40,8 @@ class Passes:
     pd: str = "3"
 
 
-KERNEL = Passes()
+ALL_PASSES = Passes()
+KERNEL = Passes(tr="2a")
 
 
 def _f32(x):

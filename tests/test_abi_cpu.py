@@ -88,18 +88,20 @@ def test_workspace_size_null_args():
 
 
 def test_workspace_size_values():
-    # 819 tokens -> 13 chunk slots.  Per (slot, value head): T as 6 split
-    # fragments (12 KiB) + 5 rows of 64 fp32 scalars; outputs add P (12 KiB).
-    # Per (slot, key head): the K record, (K, K^T [, Q]) = (16 + 16 [+ 16]) 1 KiB
-    # fragments for d_k = 128, one bf16 part for bf16 inputs, hi and lo for fp32.
-    t_rec, s_rec, frag = 6 * 2 * 1024, 5 * 64 * 4, 1024
+    # 819 tokens -> 13 chunk slots.  Per (slot, value head): T as 6 fragments,
+    # hi only for bf16 inputs (6 KiB; hi and lo for fp32, 12 KiB) + 5 rows of
+    # 64 fp32 scalars; outputs add P, split (12 KiB).  Per (slot, key head):
+    # the K record, (K, K^T [, Q]) = (16 + 16 [+ 16]) 1 KiB fragments for
+    # d_k = 128, one bf16 part for bf16 inputs, hi and lo for fp32.
+    t_rec, s_rec, frag = 6 * 1024, 5 * 64 * 4, 1024
+    p_rec = 6 * 2 * 1024
     records = 13 * 32 * (t_rec + s_rec) + 13 * 16 * 32 * frag
     st, n = _ws_size(_shape(), _cu([0, 819]))
     assert st == 0 and n == records
     st, nf = _ws_size(_shape(), _cu([0, 819]), 1)
-    assert st == 0 and nf == records + 13 * 32 * t_rec + 13 * 16 * 16 * frag
+    assert st == 0 and nf == records + 13 * 32 * p_rec + 13 * 16 * 16 * frag
     st, n32 = _ws_size(_shape(qkv_dtype=binding.GDN_F32), _cu([0, 819]))
-    assert st == 0 and n32 == records + 13 * 16 * 32 * frag
+    assert st == 0 and n32 == records + 13 * 16 * 32 * frag + 13 * 32 * t_rec
     st, n64 = _ws_size(_shape(d_k=64), _cu([0, 819]))
     assert st == 0 and n64 == 13 * 32 * (t_rec + s_rec) + 13 * 16 * 16 * frag
     # two sequences: slots cu[n]/64 + n + j, the last ends at 100/64 + 1 + 1 = 3
@@ -120,9 +122,9 @@ def test_workspace_size_values():
     # with outputs, fp32 inputs, or two sequences at 32 heads (512 split
     # workgroups, more than the chip): no split regions
     st, nlf = _ws_size(_shape(), _cu([0, 1300]), 1)
-    assert st == 0 and nlf == 21 * 32 * (2 * t_rec + s_rec) + 21 * 16 * 48 * frag
+    assert st == 0 and nlf == 21 * 32 * (t_rec + p_rec + s_rec) + 21 * 16 * 48 * frag
     st, nl32 = _ws_size(_shape(qkv_dtype=binding.GDN_F32), _cu([0, 1300]))
-    assert st == 0 and nl32 == 21 * 32 * (t_rec + s_rec) + 21 * 16 * 64 * frag
+    assert st == 0 and nl32 == 21 * 32 * (2 * t_rec + s_rec) + 21 * 16 * 64 * frag
     # slots 0..20, then 1300/64 + 1 = 21 .. 41
     st, n2l = _ws_size(_shape(num_seqs=2), _cu([0, 1300, 2600]))
     assert st == 0 and n2l == 42 * 32 * (t_rec + s_rec) + 42 * 16 * 32 * frag

@@ -248,7 +248,9 @@ def test_split_replay_agrees_with_one_chain(r, slow):
                                    cu_tail_host=x1["cu_host"], cu_suf_host=xs["cu_host"])
     e_mid = state_err(to_f64(mid), to_f64(chain[:1]))
     print(f"[split] r={r}: split vs one chain {e:.2e}, fused tail vs one chain {e_mid:.2e}", flush=True)
-    assert e <= 1e-5
+    # each form is within ~5e-4 of the exact state (bf16 inputs: hi(T) alone in
+    # T R), and the two round differently, so they differ by at most 1e-3
+    assert e <= 1e-3
     assert torch.equal(mid, chain[:1])
 
 
