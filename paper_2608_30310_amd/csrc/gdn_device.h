@@ -147,6 +147,15 @@ __device__ __forceinline__ f32x4 mma_b(const Frag& a, const Frag& b, f32x4 c) {
   return mma(a.lo, b.hi, c);
 }
 
+// ---------------------------------------------------------------- K record lane order
+// Position of lane l's 16 bytes inside a K-record fragment: within each
+// quarter of 16 lanes the positions are rotated by 4 x the quarter, so the
+// 16-byte operand reads (16 consecutive lanes of one quarter) still touch 16
+// different bank groups, while the transposing reads of K^T (lanes 16 q + 4 g
+// + m of four quarters q at once) spread over twice as many bank groups as
+// without the rotation.
+__device__ __forceinline__ int kslot(int l) { return (l & 48) | ((l + 4 * (l >> 4)) & 15); }
+
 // ---------------------------------------------------------------- k-slot permutation
 // Within a 32-wide k step, MFMA slot 8g + j (g = lane/16, j = 0..7) is mapped to
 // contraction index 4g + j for j < 4 and 16 + 4g + (j - 4) for j >= 4.  With this

@@ -14,9 +14,9 @@
 //
 // Everything is written to the workspace as ready-made MFMA A operands in the
 // order the scan consumes them (k slots permuted by kperm): T and P split into
-// bf16 hi/lo (only their six nonzero fragments), the per-row scalars and, by
-// the first value head of each key head, the K record (K, K^T and Q as
-// operands; split into hi/lo for fp32 inputs).
+// bf16 hi/lo (only their six nonzero fragments; T hi only for bf16 inputs), the
+// per-row scalars and, by the first value head of each key head, the K record
+// (K and Q as operands; split into hi/lo for fp32 inputs).
 #pragma once
 
 #include "gdn_device.h"
@@ -104,7 +104,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   constexpr int NL = S::NL;
   constexpr int AP = S::AP;
   constexpr int NK = DK / 32;
-  constexpr int NKA = ka_frags(DK), NKT = kt_frags(DK);
+  constexpr int NKA = ka_frags(DK);
   constexpr int NKF = k_record_frags(DK, FWD);   // fragments per bf16 part
   auto& Ks = sm.Ks;
   auto& Qs = sm.Qs;
@@ -250,13 +250,12 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
 #pragma unroll
     for (int i = 0; i < 16; ++i) Ts[16 * b + i][16 * b + jj] = x[i];
   } else if (h % grp == 0) {
-    // ---- meanwhile, the K record of this key head: K, K^T (and Q) as bf16 A
+    // ---- meanwhile, the K record of this key head: K (and Q) as bf16 A
     //      operands (hi and lo parts for fp32 inputs).
     //      fragment f, lane (g, r), element j:
     //        K   (ti, kk): K[16 ti + r][32 kk + kperm(g, j)]            f = ti * NK + kk
-    //        K^T (td, kk): K[32 kk + kperm(g, j)][16 td + r]            f = NKA + 2 td + kk
-    //        Q   (ti, kk): Q[16 ti + r][32 kk + kperm(g, j)]            f = NKA + NKT + ti * NK + kk
-    //      record layout [hi | lo][fragment][lane]
+    //        Q   (ti, kk): Q[16 ti + r][32 kk + kperm(g, j)]            f = NKA + ti * NK + kk
+    //      record layout [hi | lo][fragment][kslot(lane)]
     u32x4* kdst = Kw + (static_cast<int64_t>(slot) * hk + kh) * (NL * NKF * kWave);
     // Three waves share each kind of fragment; every wave first reads all of its
     // fragments (indices clamped so the reads are unconditional), then stores.
@@ -264,45 +263,29 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
       const int ti = f / NK, kk = f % NK;
       return __builtin_bit_cast(u32x4, perm_frag(&Ks[p][16 * ti + lr][32 * kk + 4 * lg]));
     };
-    auto kt_val = [&](int p, int f) __attribute__((always_inline)) {   // f < NKT
-      // two transposing reads: lane (g, r) of each 16-lane group addresses row
-      // 32 kk + 4 g + r / 4 (then 16 rows further), columns 16 td + 4 (r % 4)..+3,
-      // and receives rows 32 kk + kperm(g, j) of column 16 td + r
-      const int td = f / 2, kk = f % 2;
-      const int row = 32 * kk + 4 * lg + lr / 4, c = 16 * td + 4 * (lr % 4);
-      return __builtin_bit_cast(u32x4, join_halves(lds_read_tr16(&Ks[p][row][c]),
-                                                   lds_read_tr16(&Ks[p][row + 16][c])));
-    };
     auto q_val = [&](int p, int f) __attribute__((always_inline)) {    // f < NKA
       const int ti = f / NK, kk = f % NK;
       return __builtin_bit_cast(
           u32x4, perm_frag(&Qs[FWD ? p : 0][FWD ? 16 * ti + lr : 0][FWD ? 32 * kk + 4 * lg : 0]));
     };
-    constexpr int PA = (NKA + 2) / 3, PT = (NKT + 2) / 3;   // per wave, per part
+    constexpr int PA = (NKA + 2) / 3;                        // per wave, per part
     const int w3 = wave - 1;                                 // 0..2
 #pragma unroll
     for (int p = 0; p < NL; ++p) {
       u32x4* pdst = kdst + static_cast<int64_t>(p) * NKF * kWave;
-      u32x4 va[PA], vt[PT], vq[FWD ? PA : 1];
+      u32x4 va[PA], vq[FWD ? PA : 1];
 #pragma unroll
       for (int i = 0; i < PA; ++i) {
         va[i] = ka_val(p, min(w3 + 3 * i, NKA - 1));
         if constexpr (FWD) vq[i] = q_val(p, min(w3 + 3 * i, NKA - 1));
       }
 #pragma unroll
-      for (int i = 0; i < PT; ++i) vt[i] = kt_val(p, min(w3 + 3 * i, NKT - 1));
-#pragma unroll
       for (int i = 0; i < PA; ++i) {
         const int f = w3 + 3 * i;
         if (f < NKA) {
-          pdst[f * kWave + lane] = va[i];
-          if constexpr (FWD) pdst[(NKA + NKT + f) * kWave + lane] = vq[i];
+          pdst[f * kWave + kslot(lane)] = va[i];
+          if constexpr (FWD) pdst[(NKA + f) * kWave + kslot(lane)] = vq[i];
         }
-      }
-#pragma unroll
-      for (int i = 0; i < PT; ++i) {
-        const int f = w3 + 3 * i;
-        if (f < NKT) pdst[(NKA + f) * kWave + lane] = vt[i];
       }
     }
   }
@@ -377,8 +360,9 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
 
   // ---- T (and P) as split A fragments, nonzero ones only: fragment
   //      tri_frag(ti, kk), lane (g, r), element j = [16 ti + r][32 kk + kperm(g, j)];
-  //      record layout [hi | lo][fragment][lane]
-  u32x4* tdst = Tw + rec * (2 * kTFrags * kWave);
+  //      record layout [hi | lo][fragment][lane]; for bf16 inputs T keeps hi only
+  constexpr int TPARTS = t_record_parts(SPLIT);
+  u32x4* tdst = Tw + rec * (TPARTS * kTFrags * kWave);
   u32x4* pdst = FWD ? Pw + rec * (2 * kTFrags * kWave) : nullptr;
   for (int e = tid; e < kTFrags * kWave; e += 256) {
     const int f = e / kWave, fl = e % kWave;
@@ -395,7 +379,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
     }
     const Frag tf = split8(tv);
     tdst[e] = __builtin_bit_cast(u32x4, tf.hi);
-    tdst[kTFrags * kWave + e] = __builtin_bit_cast(u32x4, tf.lo);
+    if constexpr (TPARTS == 2) tdst[kTFrags * kWave + e] = __builtin_bit_cast(u32x4, tf.lo);
     if constexpr (FWD) {
       const Frag pf = split8(pv);
       pdst[e] = __builtin_bit_cast(u32x4, pf.hi);

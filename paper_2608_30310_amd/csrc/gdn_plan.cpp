@@ -97,7 +97,7 @@ gdn_status make_plan(const gdn_shape* shape, const int32_t* cu, bool with_output
   p.off_K = off;
   off = align_up(off + p.k_record * static_cast<size_t>(slots) * hk);
   p.off_T = off;
-  off = align_up(off + kTRecordBytes * recs);
+  off = align_up(off + t_record_bytes(shape->qkv_dtype == GDN_F32) * recs);
   p.off_S = off;
   off = align_up(off + kSRecordBytes * recs);
   p.off_P = off;

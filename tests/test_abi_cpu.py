@@ -91,43 +91,47 @@ def test_workspace_size_values():
     # 819 tokens -> 13 chunk slots.  Per (slot, value head): T as 6 fragments,
     # hi only for bf16 inputs (6 KiB; hi and lo for fp32, 12 KiB) + 5 rows of
     # 64 fp32 scalars; outputs add P, split (12 KiB).  Per (slot, key head):
-    # the K record, (K, K^T [, Q]) = (16 + 16 [+ 16]) 1 KiB fragments for
-    # d_k = 128, one bf16 part for bf16 inputs, hi and lo for fp32.
+    # the K record, K [and Q] as 4 x d_k / 32 1 KiB fragments each, one bf16
+    # part for bf16 inputs, hi and lo for fp32.
     t_rec, s_rec, frag = 6 * 1024, 5 * 64 * 4, 1024
     p_rec = 6 * 2 * 1024
-    records = 13 * 32 * (t_rec + s_rec) + 13 * 16 * 32 * frag
+
+    def krec(dk=128, outputs=False, split=False):
+        return 4 * (dk // 32) * (2 if outputs else 1) * (2 if split else 1) * frag
+
+    records = 13 * 32 * (t_rec + s_rec) + 13 * 16 * krec()
     st, n = _ws_size(_shape(), _cu([0, 819]))
     assert st == 0 and n == records
     st, nf = _ws_size(_shape(), _cu([0, 819]), 1)
-    assert st == 0 and nf == records + 13 * 32 * p_rec + 13 * 16 * 16 * frag
+    assert st == 0 and nf == 13 * 32 * (t_rec + p_rec + s_rec) + 13 * 16 * krec(outputs=True)
     st, n32 = _ws_size(_shape(qkv_dtype=binding.GDN_F32), _cu([0, 819]))
-    assert st == 0 and n32 == records + 13 * 16 * 32 * frag + 13 * 32 * t_rec
+    assert st == 0 and n32 == 13 * 32 * (2 * t_rec + s_rec) + 13 * 16 * krec(split=True)
     st, n64 = _ws_size(_shape(d_k=64), _cu([0, 819]))
-    assert st == 0 and n64 == 13 * 32 * (t_rec + s_rec) + 13 * 16 * 16 * frag
+    assert st == 0 and n64 == 13 * 32 * (t_rec + s_rec) + 13 * 16 * krec(dk=64)
     # two sequences: slots cu[n]/64 + n + j, the last ends at 100/64 + 1 + 1 = 3
     st, n2 = _ws_size(_shape(num_seqs=2), _cu([0, 100, 130]))
-    assert st == 0 and n2 == 3 * 32 * (t_rec + s_rec) + 3 * 16 * 32 * frag
+    assert st == 0 and n2 == 3 * 32 * (t_rec + s_rec) + 3 * 16 * krec()
     # the longest-first order travels in the kernels' arguments: no region
     st, n2u = _ws_size(_shape(num_seqs=2), _cu([0, 30, 130]))
-    assert st == 0 and n2u == 3 * 32 * (t_rec + s_rec) + 3 * 16 * 32 * frag
+    assert st == 0 and n2u == 3 * 32 * (t_rec + s_rec) + 3 * 16 * krec()
     # Tail replay of bf16 inputs that may run in two halves (at least 20
     # chunks, N x Hv x (d_v / 32 + (d_v + d_k) / 64) <= 256 workgroups) adds
     # the second half's fp32 state [N, Hv, d_k, d_v] and transition [N, Hv,
     # d_k, d_k]: 1300 tokens -> 21 slots
     st, nl = _ws_size(_shape(), _cu([0, 1300]))
-    assert st == 0 and nl == 21 * 32 * (t_rec + s_rec) + 21 * 16 * 32 * frag + 32 * 128 * 128 * 4 * 2
+    assert st == 0 and nl == 21 * 32 * (t_rec + s_rec) + 21 * 16 * krec() + 32 * 128 * 128 * 4 * 2
     st, nl64 = _ws_size(_shape(d_k=64), _cu([0, 1300]))
-    assert st == 0 and nl64 == (21 * 32 * (t_rec + s_rec) + 21 * 16 * 16 * frag
+    assert st == 0 and nl64 == (21 * 32 * (t_rec + s_rec) + 21 * 16 * krec(dk=64)
                                 + 32 * 64 * 128 * 4 + 32 * 64 * 64 * 4)
     # with outputs, fp32 inputs, or two sequences at 32 heads (512 split
     # workgroups, more than the chip): no split regions
     st, nlf = _ws_size(_shape(), _cu([0, 1300]), 1)
-    assert st == 0 and nlf == 21 * 32 * (t_rec + p_rec + s_rec) + 21 * 16 * 48 * frag
+    assert st == 0 and nlf == 21 * 32 * (t_rec + p_rec + s_rec) + 21 * 16 * krec(outputs=True)
     st, nl32 = _ws_size(_shape(qkv_dtype=binding.GDN_F32), _cu([0, 1300]))
-    assert st == 0 and nl32 == 21 * 32 * (2 * t_rec + s_rec) + 21 * 16 * 64 * frag
+    assert st == 0 and nl32 == 21 * 32 * (2 * t_rec + s_rec) + 21 * 16 * krec(split=True)
     # slots 0..20, then 1300/64 + 1 = 21 .. 41
     st, n2l = _ws_size(_shape(num_seqs=2), _cu([0, 1300, 2600]))
-    assert st == 0 and n2l == 42 * 32 * (t_rec + s_rec) + 42 * 16 * 32 * frag
+    assert st == 0 and n2l == 42 * 32 * (t_rec + s_rec) + 42 * 16 * krec()
     st, z = _ws_size(_shape(num_seqs=0), _cu([0]))
     assert st == 0 and z < 1024
     assert gdn.workspace_size(1, 16, 32, 128, 128, [0, 819]) == n
