@@ -232,6 +232,34 @@ gdn_status gdn_decode_step(const gdn_shape* shape,
                            void* stream);
 
 /*
+ * Tail replay that allocates nothing, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same operation, arguments, layouts and results as
+ * gdn_tail_replay (the same kernels, so the states are bit for bit equal),
+ * but the workspace is a device array inside the library of
+ * GDN_NOALLOC_SCRATCH_BYTES bytes, one copy per GPU, held until the process
+ * ends; the caller still owns k, v, g, beta and state_out.  Inputs whose
+ * workspace (gdn_workspace_size(..., 0, ...)) exceeds the array are rejected
+ * with GDN_ERR_WORKSPACE before anything is enqueued.  The array's device
+ * address is looked up on the first call on each device (the current device
+ * at the call); no call allocates, frees or synchronises.  Every call on one
+ * GPU shares that GPU's array: calls that may overlap on one GPU (on
+ * different streams, or from several threads without ordering) race and give
+ * wrong results; order them on one stream.
+ */
+#define GDN_NOALLOC_SCRATCH_BYTES (64u << 20)
+gdn_status gdn_tail_replay_noalloc(const gdn_shape* shape,
+                                   const int32_t* cu_seqlens_host,
+                                   const int32_t* cu_seqlens,
+                                   const void* k, const void* v,
+                                   const float* g, const float* beta,
+                                   float* state_out,
+                                   void* stream);
+
+/* GDN_NOALLOC_SCRATCH_BYTES, as the library was built. */
+size_t gdn_noalloc_scratch_bytes(void);
+
+/*
  * Replay budget of the paper (Section 3): k = ceil(r * m) for a ratio
  * r = ratio_num / ratio_den, in exact integer arithmetic.  Returns -1 when
  * m < 0, ratio_num < 0, ratio_den <= 0 or the product overflows.

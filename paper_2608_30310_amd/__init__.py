@@ -12,11 +12,11 @@ cached hiddens as well.  The work runs in hand-written HIP kernels for gfx950
 a thin binding of that library.
 """
 from .binding import (GDNError, LIB_PATH, chunk_forward, decode_step, la_block_replay,
-                      la_block_stage_names, la_block_workspace_size, load_library, replay_forward,
-                      replay_forward_stage_names, replay_forward_workspace_size, replay_len,
-                      stage_names, tail_replay, workspace_size)
+                      la_block_stage_names, la_block_workspace_size, load_library, noalloc_scratch_bytes,
+                      replay_forward, replay_forward_stage_names, replay_forward_workspace_size,
+                      replay_len, stage_names, tail_replay, tail_replay_noalloc, workspace_size)
 
 __all__ = ["GDNError", "LIB_PATH", "chunk_forward", "decode_step", "la_block_replay",
-           "la_block_stage_names", "la_block_workspace_size", "load_library", "replay_forward",
-           "replay_forward_stage_names", "replay_forward_workspace_size", "replay_len",
-           "stage_names", "tail_replay", "workspace_size"]
+           "la_block_stage_names", "la_block_workspace_size", "load_library", "noalloc_scratch_bytes",
+           "replay_forward", "replay_forward_stage_names", "replay_forward_workspace_size", "replay_len",
+           "stage_names", "tail_replay", "tail_replay_noalloc", "workspace_size"]

@@ -89,6 +89,10 @@ def load_library():
     lib.gdn_num_stages.restype = ctypes.c_int32
     lib.gdn_stage_name.argtypes = [ctypes.c_int32, ctypes.c_int32]
     lib.gdn_stage_name.restype = ctypes.c_char_p
+    lib.gdn_tail_replay_noalloc.argtypes = [SP, P, P, P, P, P, P, P, P]
+    lib.gdn_tail_replay_noalloc.restype = ctypes.c_int
+    lib.gdn_noalloc_scratch_bytes.argtypes = []
+    lib.gdn_noalloc_scratch_bytes.restype = ctypes.c_size_t
     lib.gdn_decode_step.argtypes = [SP, P, P, P, P, P, P, P, P, P]
     lib.gdn_decode_step.restype = ctypes.c_int
     LP = ctypes.POINTER(LAShape)
@@ -283,6 +287,48 @@ def tail_replay(k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, beta: torch.T
     else:
         arr, n = _event_array(events, False)
         _check(lib.gdn_tail_replay_profiled(*args, ctypes.cast(arr, ctypes.c_void_p), n))
+    return state_out
+
+
+def noalloc_scratch_bytes() -> int:
+    """Size of the device array ``tail_replay_noalloc`` uses as its workspace."""
+    return int(load_library().gdn_noalloc_scratch_bytes())
+
+
+def tail_replay_noalloc(k: torch.Tensor, v: torch.Tensor, g: torch.Tensor, beta: torch.Tensor,
+                        cu_seqlens, cu_seqlens_host, state_out: torch.Tensor) -> torch.Tensor:
+    """``tail_replay`` through ``gdn_tail_replay_noalloc``: the library takes
+    its workspace from a device array of its own and allocates nothing; the
+    caller passes every tensor, including ``state_out`` [N, Hv, d_k, d_v] fp32
+    and the device and host copies of ``cu_seqlens``.  Calls that may overlap
+    on one GPU share that array and must be ordered on one stream."""
+    lib = load_library()
+    device = k.device
+    dt = k.dtype
+    _need(k, "k", dt, device, 3)
+    _need(v, "v", dt, device, 3)
+    T, hk, dk = k.shape
+    hv, dv = v.shape[1], v.shape[2]
+    if v.shape[0] != T:
+        raise ValueError("k and v must hold the same tokens")
+    _need(g, "g", torch.float32, device, 2)
+    _need(beta, "beta", torch.float32, device, 2)
+    if tuple(g.shape) != (T, hv) or tuple(beta.shape) != (T, hv):
+        raise ValueError("g and beta must be [T, Hv]")
+    if not isinstance(cu_seqlens, torch.Tensor) or cu_seqlens.device != device:
+        raise ValueError("cu_seqlens must be a device tensor (nothing is copied here)")
+    if not isinstance(cu_seqlens_host, torch.Tensor):
+        raise ValueError("cu_seqlens_host must be a host tensor")
+    cu_dev, cu_host = _seqlens(cu_seqlens, cu_seqlens_host, device)
+    n = cu_host.numel() - 1
+    _need(state_out, "state_out", torch.float32, device, 4)
+    if tuple(state_out.shape) != (n, hv, dk, dv):
+        raise ValueError("state_out must be [N, Hv, d_k, d_v]")
+    shp = _shape(n, hk, hv, dk, dv, _dtype_code(k), 1.0)
+    stream = torch.cuda.current_stream(device)
+    _check(lib.gdn_tail_replay_noalloc(ctypes.byref(shp), _ptr(cu_host), _ptr(cu_dev), _ptr(k), _ptr(v),
+                                       _ptr(g), _ptr(beta), _ptr(state_out),
+                                       ctypes.c_void_p(stream.cuda_stream)))
     return state_out
 
 

@@ -20,6 +20,7 @@
 #include <cstdint>
 #include <cstring>
 #include <limits>
+#include <mutex>
 #include <string>
 
 #include "gdn_decode.h"
@@ -489,6 +490,68 @@ gdn_status decode_step_impl(const gdn_shape* shape, const void* q, const void* k
 }  // namespace
 }  // namespace gdn
 
+namespace gdn {
+namespace {
+
+// ---------------------------------------------------------------- replay without allocation
+// Workspace of gdn_tail_replay_noalloc: a file-scope device array, one copy
+// per GPU the library runs on, held until the process ends.  In host code
+// `scratch` only names the symbol; its device address on each GPU comes from
+// hipGetSymbolAddress on that GPU's first call and is kept per device.
+constexpr size_t kNoAllocScratchBytes = size_t{GDN_NOALLOC_SCRATCH_BYTES};
+static_assert(kNoAllocScratchBytes % kAlign == 0, "scratch size");
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[kMaxScratchDevices] = {};
+
+// The scratch array's address on the current device.
+gdn_status scratch_on_current_device(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(GDN_ERR_HIP, std::string("hipGetDevice: ") + hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxScratchDevices)
+    return fail(GDN_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr)
+      return fail(GDN_ERR_HIP, std::string("hipGetSymbolAddress(scratch): ") + hipGetErrorString(e));
+    if (reinterpret_cast<uintptr_t>(ptr) % kAlign != 0)
+      return fail(GDN_ERR_HIP, "scratch array is not 256-byte aligned");
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return GDN_OK;
+}
+
+gdn_status tail_replay_noalloc_impl(const gdn_shape* shape, const int32_t* cu_seqlens_host,
+                                    const int32_t* cu_seqlens, const void* k, const void* v, const float* g,
+                                    const float* beta, float* state_out, void* stream) {
+  // the plan first: an input too large for the scratch array is rejected
+  // before anything touches the device
+  Plan plan;
+  std::string err;
+  const gdn_status st = make_plan(shape, cu_seqlens_host, false, &plan, &err);
+  if (st != GDN_OK) return fail(st, err);
+  if (plan.bytes > kNoAllocScratchBytes)
+    return fail(GDN_ERR_WORKSPACE, "input needs " + std::to_string(plan.bytes) +
+                                       " workspace bytes, more than the no-allocation scratch array holds (" +
+                                       std::to_string(kNoAllocScratchBytes) + ")");
+  void* ws = nullptr;
+  if (shape->num_seqs > 0 && plan.bytes > 0) {
+    const gdn_status sst = scratch_on_current_device(&ws);
+    if (sst != GDN_OK) return sst;
+  }
+  return tail_replay_impl(shape, cu_seqlens_host, cu_seqlens, k, v, g, beta, state_out, ws,
+                          ws ? kNoAllocScratchBytes : 0, stream, nullptr);
+}
+
+}  // namespace
+}  // namespace gdn
+
 extern "C" {
 
 gdn_status gdn_tail_replay(const gdn_shape* shape, const int32_t* cu_seqlens_host,
@@ -498,6 +561,14 @@ gdn_status gdn_tail_replay(const gdn_shape* shape, const int32_t* cu_seqlens_hos
   return gdn::tail_replay_impl(shape, cu_seqlens_host, cu_seqlens, k, v, g, beta, state_out,
                                workspace, workspace_bytes, stream, nullptr);
 }
+
+gdn_status gdn_tail_replay_noalloc(const gdn_shape* shape, const int32_t* cu_seqlens_host,
+                                   const int32_t* cu_seqlens, const void* k, const void* v, const float* g,
+                                   const float* beta, float* state_out, void* stream) {
+  return gdn::tail_replay_noalloc_impl(shape, cu_seqlens_host, cu_seqlens, k, v, g, beta, state_out, stream);
+}
+
+size_t gdn_noalloc_scratch_bytes(void) { return gdn::kNoAllocScratchBytes; }
 
 gdn_status gdn_tail_replay_profiled(const gdn_shape* shape, const int32_t* cu_seqlens_host,
                                     const int32_t* cu_seqlens, const void* k, const void* v,

@@ -275,3 +275,21 @@ def test_replay_forward_rejects_before_launch(case):
                                 out.value - (256 if case == "small_ws" else 0), None)
     want = {"null_mid": 1, "null_o": 1, "misaligned_k_tail": 4, "small_ws": 5, "overlap": 2}[case]
     assert st == want, lib.gdn_last_error().decode()
+
+
+def test_noalloc_rejects_input_beyond_its_scratch_before_any_device_call():
+    # the plan comes first: an input whose workspace exceeds the library's
+    # scratch array returns GDN_ERR_WORKSPACE without touching the device
+    lib = gdn.load_library()
+    assert lib.gdn_noalloc_scratch_bytes() == 64 << 20 == gdn.noalloc_scratch_bytes()
+    shape = _shape(num_seqs=1)
+    big = _cu([0, 60000])          # ~0.5 GiB of records at 32 heads
+    _, need = _ws_size(shape, big)
+    assert need > 64 << 20
+    st = lib.gdn_tail_replay_noalloc(ctypes.byref(shape), ctypes.cast(big, ctypes.c_void_p), FAKE, FAKE, FAKE,
+                                     FAKE, FAKE, FAKE, None)
+    assert st == 5 and b"scratch" in lib.gdn_last_error()
+    # and the ordinary validation still applies
+    st = lib.gdn_tail_replay_noalloc(ctypes.byref(_shape(num_seqs=2)), ctypes.cast(_cu([0, 10, 5]), ctypes.c_void_p),
+                                     FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None)
+    assert st == 3
