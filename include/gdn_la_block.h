@@ -42,8 +42,10 @@
  * Conventions as in gdn_tail_replay.h (caller-owned buffers and workspace,
  * host-side validation before anything is enqueued, everything on `stream`),
  * with two additions: the first call on a device creates that device's
- * hipBLASLt handle, kept until the process ends (the projections run through
- * hipBLASLt; their workspace is part of the caller's), and `out` may alias
+ * hipBLASLt handle, kept until the process ends, and the matmul descriptors
+ * and algorithm choice of each projection shape are cached with it (at most
+ * 512 shapes; beyond that they are prepared per call) (the projections run
+ * through hipBLASLt; their workspace is part of the caller's), and `out` may alias
  * `x` (x is read only by the in-projection, before out is written).  To
  * capture calls in a HIP graph, make one eager call of the same shape first
  * (the handle and the projections' algorithm choice are set up on it).
