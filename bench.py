@@ -11,10 +11,13 @@ Default workload: a stack of 36 GDN layers with hybrid-model head shapes
 each with its own seeded inputs; matched prefix 32768 tokens, replay tail 3277
 tokens (10 %), 1024 new suffix tokens.  The step runs the layers one after the
 other, as the layers of a group depend on each other (paper Section 3): per
-layer ``gdn_tail_replay`` then ``gdn_chunk_forward`` from the rebuilt state,
-launched eagerly on one stream.  ``value`` = tokens through the path per
-second, 36 x (3277 + 1024) per step.  Beside it: the same step replayed from a
-HIP graph, the 36 layers as one batched call (layers as sequences), the
+layer one ``gdn_replay_forward`` call (the tail replay, then the suffix forward
+from the rebuilt state; the suffix's chunk preparation runs beside the tail's
+scan), launched eagerly on one stream.  ``value`` = tokens through the path per
+second, 36 x (3277 + 1024) per step.  Beside it: the same step as two calls
+per layer (``gdn_tail_replay`` + ``gdn_chunk_forward``, bit for bit the same
+results) and replayed from a HIP graph, the 36 layers as one batched call
+(layers as sequences), the
 rebuild latency of the 36 replays (warm, cold, queued), per-stage kernel
 durations from HIP events that the library records on the stream its kernels
 run on, ``roofline`` for the dominant kernel, the one-layer workload
@@ -305,7 +308,9 @@ def main():
     ws_t = torch.empty(gdn.workspace_size(1, hk, hv, dk, dv, cu_t1) + 256, dtype=torch.uint8, device=dev)
     ws_f = torch.empty(gdn.workspace_size(1, hk, hv, dk, dv, cu_s1, with_outputs=True) + 256,
                        dtype=torch.uint8, device=dev)
-    names_t, names_f = gdn.stage_names(False), gdn.stage_names(True)
+    ws_rf = torch.empty(gdn.replay_forward_workspace_size(1, hk, hv, dk, dv, cu_t1, cu_s1) + 256,
+                        dtype=torch.uint8, device=dev)
+    names_rf = gdn.replay_forward_stage_names()
 
     def replay_layer(l, ev=None):
         x = lt[l]
@@ -317,10 +322,20 @@ def main():
         gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], cu_s1_d, cu_s1_h, state_in=mid[l:l + 1],
                           o=o[l * s:(l + 1) * s], state_out=fin[l:l + 1], workspace=ws_f, events=ev)
 
+    def fused_layer(l, ev=None):
+        a, b = lt[l], ls[l]
+        gdn.replay_forward(a["k"], a["v"], a["g"], a["beta"], cu_t1_d, b["q"], b["k"], b["v"], b["g"], b["beta"],
+                           cu_s1_d, cu_tail_host=cu_t1_h, cu_suf_host=cu_s1_h, state_mid=mid[l:l + 1],
+                           o=o[l * s:(l + 1) * s], state_out=fin[l:l + 1], workspace=ws_rf, events=ev)
+
     def step(evs=None):
         for l in range(L):
-            replay_layer(l, evs[l][0] if evs else None)
-            forward_layer(l, evs[l][1] if evs else None)
+            fused_layer(l, evs[l] if evs else None)
+
+    def two_calls_step():
+        for l in range(L):
+            replay_layer(l)
+            forward_layer(l)
 
     def rebuild():
         for l in range(L):
@@ -386,13 +401,18 @@ def main():
             graph = g
         else:
             graph_note = "graph replay differed from the eager step; graph not timed"
-    # the batched form computes the same states up to rounding order
+    # the two calls give the fused call's results bit for bit; the batched
+    # form the same states up to rounding order
+    two_calls_step()
+    torch.cuda.synchronize()
+    two_calls_equal = bool(torch.equal(mid, want[0]) and torch.equal(fin, want[1]) and torch.equal(o, want[2]))
     batched_step()
     torch.cuda.synchronize()
     bdiff = float(((finb - want[1]).norm() / want[1].norm()).item())
 
     ms_per_step = timed(step)
     ms_graph = timed(graph.replay) if graph is not None else None
+    ms_two_calls = timed(two_calls_step)
     ms_batched = timed(batched_step)
     ms_batched_rebuild = timed(batched_replay)
 
@@ -405,19 +425,16 @@ def main():
             e.record()
         return evs
 
-    evs = [[(new_events(len(names_t) + 1), new_events(len(names_f) + 1)) for _ in range(L)] for _ in range(n_ev)]
+    evs = [[new_events(len(names_rf) + 1) for _ in range(L)] for _ in range(n_ev)]
     torch.cuda.synchronize()
     for i in range(n_ev):
         step(evs[i])
     torch.cuda.synchronize()
     stages = {}
-    for part, names in ((0, names_t), (1, names_f)):
-        prefix = ("tail_replay.", "chunk_forward.")[part]
-        for j, nm in enumerate(names):
-            d = [evs[i][l][part][j].elapsed_time(evs[i][l][part][j + 1]) * 1e3
-                 for i in range(n_ev) for l in range(L)]
-            stages[prefix + nm] = {"mean_us": statistics.fmean(d), "median_us": statistics.median(d),
-                                   "per_step_us": statistics.fmean(d) * L}
+    for j, nm in enumerate(names_rf):
+        d = [evs[i][l][j].elapsed_time(evs[i][l][j + 1]) * 1e3 for i in range(n_ev) for l in range(L)]
+        stages["replay_forward." + nm] = {"mean_us": statistics.fmean(d), "median_us": statistics.median(d),
+                                          "per_step_us": statistics.fmean(d) * L}
 
     # ---- rebuild latency of the stack (the 36 replays): warm (from an idle
     #      stream), queued (a spin kernel holds the GPU while the host enqueues,
@@ -470,17 +487,23 @@ def main():
     # bytes are those of the part of the path it runs, per launch (one layer)
     dom = max(stages, key=lambda k: stages[k]["per_step_us"])
     grp = hv // hk
-    split = stages["tail_replay.combine"]["mean_us"] > 0.5
+    split = stages["replay_forward.combine (+ suffix intra)"]["mean_us"] > 0.5
+    # the suffix's chunk preparation reads q, k (shared by the group), g and
+    # beta and forms K K^T and Q K^T per chunk; the combine reads the
+    # transition, the second half's state and the first half's, and writes
+    # the state
+    prep_bytes = s * hv * (2 * elt * dk / grp + 8)
+    prep_flops = s * hv * (2 * 2 * CHUNK * dk / grp)
+    comb_bytes, comb_flops = 3 * state_bytes + hv * dk * dk * 4, 2 * hv * dk * dk * dv
     kinfo = {
-        "tail_replay.intra": ("gdn::k_intra<unsigned short, 128, false>",
-                              r * hv * (elt * dk / grp + 8), r * hv * 2 * CHUNK * dk / grp),
-        "tail_replay.scan": ("gdn::k_scan_cols_split<unsigned short, 128>" if split
-                             else "gdn::k_scan_cols<unsigned short, 128, false>", tail_bytes, tail_flops),
-        "tail_replay.combine": ("gdn::k_state_combine<128>", 3 * state_bytes + hv * dk * dk * 4,
-                                2 * hv * dk * dk * dv),
-        "chunk_forward.intra": ("gdn::k_intra<unsigned short, 128, true>",
-                                s * hv * (2 * elt * dk / grp + 8), s * hv * 2 * 2 * CHUNK * dk / grp),
-        "chunk_forward.scan": ("gdn::k_scan_cols<unsigned short, 128, true>", fwd_bytes, fwd_flops),
+        "replay_forward.tail intra": ("gdn::k_intra<unsigned short, 128, false>",
+                                      r * hv * (elt * dk / grp + 8), r * hv * 2 * CHUNK * dk / grp),
+        "replay_forward.tail scan (+ suffix intra)":
+            ("gdn::k_scan_cols_split<unsigned short, 128>", tail_bytes, tail_flops) if split else
+            ("gdn::k_scan_cols_intra<unsigned short, 128>", tail_bytes + prep_bytes, tail_flops + prep_flops),
+        "replay_forward.combine (+ suffix intra)": ("gdn::k_combine_intra<unsigned short, 128>",
+                                                    comb_bytes + prep_bytes, comb_flops + prep_flops),
+        "replay_forward.suffix scan": ("gdn::k_scan_cols<unsigned short, 128, true>", fwd_bytes, fwd_flops),
     }
     kname, kbytes, kflops = kinfo[dom]
     dom_s = stages[dom]["mean_us"] * 1e-6
@@ -509,8 +532,11 @@ def main():
                                                               f"36-layer workload",
                    "layers": L, "prefix": hits[0].m, "tail": r, "suffix": s,
                    "global_batch": L, "seq_len": r + s, "parallelism": "single GPU"},
-        "launch": "eager; per layer gdn_tail_replay then gdn_chunk_forward, layers in sequence",
+        "launch": "eager; per layer one gdn_replay_forward call (tail replay, then the suffix forward from "
+                  "the rebuilt state), layers in sequence",
         "ms_per_step_graph": ms_graph,
+        "ms_per_step_two_calls": ms_two_calls,
+        "two_calls_bitwise_equal": two_calls_equal,
         "ms_per_step_batched": ms_batched,
         "batched_vs_sequential_rel_state_diff": bdiff,
         "rebuild_latency_us": warm["p50"],

@@ -167,9 +167,12 @@ const char* gdn_stage_name(int32_t with_outputs, int32_t stage);
  * call does what gdn_tail_replay followed by gdn_chunk_forward(state_in =
  * state_mid) does, but overlaps work that does not depend on the rebuilt
  * state: the suffix's per-chunk preparation runs beside the tail's sequential
- * scan.  The tail always runs as one chain, so the results are bit for bit
- * those of the two calls wherever gdn_tail_replay runs one chain too, and
- * equal to rounding order where it splits a long tail in two halves.
+ * scan.  The tail runs in two halves exactly where gdn_tail_replay would, so
+ * the results are bit for bit those of the two calls.  Stages (for
+ * gdn_replay_forward_profiled): "tail intra", "tail scan (+ suffix intra)",
+ * "combine (+ suffix intra)", "suffix scan": the suffix's chunk preparation
+ * runs beside the tail scan when the tail is one chain, beside the combine of
+ * its two halves otherwise (the combine stage is empty for one chain).
  *   tail   (sequence n = the last r_n matched tokens, packed by cu_tail):
  *          k_tail [Tt,Hk,d_k], v_tail [Tt,Hv,d_v], g_tail, beta_tail [Tt,Hv];
  *   suffix (the new tokens of sequence n, packed by cu_suf, same N):

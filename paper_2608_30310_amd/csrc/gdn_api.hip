@@ -301,9 +301,12 @@ gdn_status chunk_forward_impl(const gdn_shape* shape, const int32_t* cu_seqlens_
 }
 
 // ---------------------------------------------------------------- replay then forward
-constexpr int32_t kNumFusedStages = 3;
-const char* const kFusedStageNames[kNumFusedStages] = {"tail intra", "tail scan + suffix intra",
-                                                       "suffix scan"};
+constexpr int32_t kNumFusedStages = 4;
+// The suffix's chunk preparation runs in the tail-scan stage when the tail is
+// one chain (on the CUs the scan leaves idle) and in the combine stage when it
+// runs in two halves (beside the combine); the combine stage is otherwise empty.
+const char* const kFusedStageNames[kNumFusedStages] = {"tail intra", "tail scan (+ suffix intra)",
+                                                       "combine (+ suffix intra)", "suffix scan"};
 
 struct FusedArgs {
   const gdn_shape* s;
@@ -349,8 +352,34 @@ gdn_status run_fused(const FusedArgs& a) {
   if ((st = fmark(a, 1)) != GDN_OK) return st;
   bool fits = false;
   uint32_t n_scan = 0;
-  if ((st = cols_fit(s, &fits, &n_scan)) != GDN_OK) return st;
-  if (fits && ps.num_slots > 0) {
+  int cus = 0;
+  if ((st = cols_fit(s, &fits, &n_scan, &cus)) != GDN_OK) return st;
+  constexpr bool kCanSplit = sizeof(TIn) == 2;   // the split form is bf16 tail replay
+  bool combine = false;
+  if (kCanSplit && pt.split && split_groups(s) <= cus && ps.num_slots > 0) {
+    // the tail in two halves (as gdn_tail_replay runs it), then its combine
+    // with the suffix's records built beside it
+    hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
+                       dim3(cols_wide_threads()), 0, a.stream, static_cast<int32_t>(split_first_groups(s)), a.cu_t,
+                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v_t),
+                       reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
+                       reinterpret_cast<const u32x4*>(a.ws_t + pt.off_T),
+                       reinterpret_cast<const float*>(a.ws_t + pt.off_S), a.state_mid,
+                       reinterpret_cast<float*>(a.ws_t + pt.off_M2), reinterpret_cast<float*>(a.ws_t + pt.off_A2));
+    if ((st = check_launch("split scan launch")) != GDN_OK) return st;
+    if ((st = fmark(a, 2)) != GDN_OK) return st;
+    const uint32_t n_comb = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCombineCols);
+    const uint32_t blocks = n_comb + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
+    hipLaunchKernelGGL((k_combine_intra<TIn, DK>), dim3(blocks), dim3(kCombineThreads), 0, a.stream,
+                       static_cast<int32_t>(n_comb), s.d_v, reinterpret_cast<const float*>(a.ws_t + pt.off_A2),
+                       reinterpret_cast<const float*>(a.ws_t + pt.off_M2), a.state_mid,
+                       static_cast<int32_t>(ps.num_slots), a.cu_s, s.num_seqs, s.num_k_heads, s.num_v_heads,
+                       static_cast<const TIn*>(a.q), static_cast<const TIn*>(a.k), a.g, a.beta, s.scale,
+                       reinterpret_cast<u32x4*>(a.ws_s + ps.off_K), reinterpret_cast<u32x4*>(a.ws_s + ps.off_T),
+                       reinterpret_cast<float*>(a.ws_s + ps.off_S), reinterpret_cast<u32x4*>(a.ws_s + ps.off_P));
+    if ((st = check_launch("combine + suffix intra launch")) != GDN_OK) return st;
+    combine = true;
+  } else if (fits && ps.num_slots > 0) {
     // the suffix's records are built on the CUs the tail replay leaves idle
     const uint32_t blocks = n_scan + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
     hipLaunchKernelGGL((k_scan_cols_intra<TIn, DK>), dim3(blocks), dim3(4 * kWave), 0, a.stream,
@@ -370,11 +399,12 @@ gdn_status run_fused(const FusedArgs& a) {
     if ((st = launch_intra<TIn, DK, true>(s, ps, a.cu_s, a.q, a.k, a.g, a.beta, a.ws_s, a.stream)) != GDN_OK)
       return st;
   }
-  if ((st = fmark(a, 2)) != GDN_OK) return st;
+  if (!combine && (st = fmark(a, 2)) != GDN_OK) return st;
+  if ((st = fmark(a, 3)) != GDN_OK) return st;
   if ((st = launch_scan<TIn, DK, DV, true>(s, ps, a.cu_s, a.v, a.state_mid, a.o, a.state_out, a.ws_s,
                                            a.stream)) != GDN_OK)
     return st;
-  return fmark(a, 3);
+  return fmark(a, 4);
 }
 
 template <int DK, int DV>

@@ -84,8 +84,10 @@ struct IntraLds {
   static_assert(sizeof(float[4][16][17]) <= sizeof(uint16_t[NL][kChunk][KP]), "block scratch fits in the keys");
 };
 
-// One intra workgroup (256 threads) for chunk slot `slot` and value head `h`,
-// with its LDS in `sm`.
+// One intra workgroup for chunk slot `slot` and value head `h`, with its LDS
+// in `sm`.  The work is laid out for four waves (256 threads); a workgroup
+// launched with more (the split scan's 320-thread launch shares its grid with
+// these) leaves the extra waves idle except for the barriers.
 template <typename TIn, int DK, bool FWD>
 __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot, int h,
                                            const int32_t* __restrict__ cu, int32_t num_seqs,
@@ -127,8 +129,9 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   int seq, start, len;
   if (!slot_owner(cu, num_seqs, slot, seq, start, len)) return;   // uniform over the block
 
+  constexpr int kWork = 4;   // waves that work
   // ---- all global loads first: K (and Q) rows, this head's gates and betas
-  {
+  if (wave < kWork) {
     const int64_t off = (static_cast<int64_t>(start) * hk + kh) * DK;
     RowTile<TIn, DK> kt, qt;
     kt.load(k + off, static_cast<int64_t>(hk) * DK, len, tid);
@@ -160,7 +163,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   //      then the MFMAs, then the elementwise pass.
   constexpr int TPW = 3;   // tiles of K K^T per wave, at most
   f32x4 pkeep[TPW];        // this wave's tiles of P until the queries are dead
-  {
+  if (wave < kWork) {
     Frag fa[TPW][NK], fb[TPW][NK], fq[TPW][NK];
     f32x4 acc[TPW], accq[TPW];
     auto tile_rc = [](int t, int& bi, int& bj) __attribute__((always_inline)) {
@@ -249,7 +252,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
       for (int i = m + 1; i < 16; ++i) x[i] -= arow[i][m / 4][m % 4] * x[m];
 #pragma unroll
     for (int i = 0; i < 16; ++i) Ts[16 * b + i][16 * b + jj] = x[i];
-  } else if (h % grp == 0) {
+  } else if (wave < kWork && h % grp == 0) {
     // ---- meanwhile, the K record of this key head: K (and Q) as bf16 A
     //      operands (hi and lo parts for fp32 inputs).
     //      fragment f, lane (g, r), element j:
@@ -291,7 +294,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   }
   __syncthreads();
 
-  if constexpr (FWD) {
+  if (FWD && wave < kWork) {
     // the Q record is written: P goes where the queries were
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
@@ -338,7 +341,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   // rows 32..63, columns 0..31: wave w owns block (rr, cc) = (2 + w / 2, w % 2);
   // first Y = A[32:64, 0:32] T[0:32, 0:32] (T_kc = 0 for k < c) ...
   const int rr = 2 + wave / 2, cc = wave % 2;
-  {
+  if (wave < kWork) {
     f32x4 y = zero4();
 #pragma unroll
     for (int k = 0; k < 2; ++k)
@@ -348,7 +351,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   }
   __syncthreads();
   // ... then -T[32:64, 32:64] Y (T_rk = 0 for k > r)
-  {
+  if (wave < kWork) {
     f32x4 xx = zero4();
 #pragma unroll
     for (int k = 2; k < 4; ++k)
@@ -364,7 +367,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   constexpr int TPARTS = t_record_parts(SPLIT);
   u32x4* tdst = Tw + rec * (TPARTS * kTFrags * kWave);
   u32x4* pdst = FWD ? Pw + rec * (2 * kTFrags * kWave) : nullptr;
-  for (int e = tid; e < kTFrags * kWave; e += 256) {
+  for (int e = tid; wave < kWork && e < kTFrags * kWave; e += kWork * kWave) {
     const int f = e / kWave, fl = e % kWave;
     const int ti = f < 2 ? f : 2 + (f - 2) / 2, kk = f < 2 ? 0 : (f - 2) % 2;
     const int fg = fl / 16, fr = fl % 16;

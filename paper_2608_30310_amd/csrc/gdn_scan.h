@@ -961,17 +961,22 @@ void k_scan_cols_split(int32_t n_first, const int32_t* __restrict__ cu, int32_t 
 constexpr int kCombineThreads = 256;
 constexpr int kCombineCols = 16;
 template <int DK>
-__global__ __launch_bounds__(kCombineThreads)
-void k_state_combine(int32_t dv, const float* __restrict__ At, const float* __restrict__ B,
-                     float* __restrict__ state) {
+struct CombineLds {
+  alignas(16) float as[DK * DK];
+  alignas(16) float ms[DK * kCombineCols];
+};
+
+template <int DK>
+__device__ __forceinline__ void combine_body(CombineLds<DK>& sm, int block, int32_t dv, const float* __restrict__ At,
+                                             const float* __restrict__ B, float* __restrict__ state) {
   constexpr int PER = DK * kCombineCols / kCombineThreads;   // staged column values per thread
   constexpr int AV = DK * DK / 4 / kCombineThreads;          // 16-byte pieces of A^T per thread
   constexpr int TILES = DK / 16 / (kCombineThreads / kWave);  // row tiles per wave
-  __shared__ __attribute__((aligned(16))) float as[DK * DK];
-  __shared__ __attribute__((aligned(16))) float ms[DK * kCombineCols];
+  float* as = sm.as;
+  float* ms = sm.ms;
   const int groups = dv / kCombineCols;
-  const int64_t head = blockIdx.x / groups;
-  const int c0 = kCombineCols * (blockIdx.x % groups);
+  const int64_t head = block / groups;
+  const int c0 = kCombineCols * (block % groups);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int li = lane % 16, lk = lane / 16;
   float* st = state + head * DK * dv + c0;
@@ -1009,6 +1014,42 @@ void k_state_combine(int32_t dv, const float* __restrict__ At, const float* __re
   for (int t = 0; t < TILES; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) st[static_cast<int64_t>(16 * (wave + 4 * t) + 4 * lk + i) * dv + li] = acc[t][i];
+}
+
+template <int DK>
+__global__ __launch_bounds__(kCombineThreads)
+void k_state_combine(int32_t dv, const float* __restrict__ At, const float* __restrict__ B,
+                     float* __restrict__ state) {
+  __shared__ CombineLds<DK> sm;
+  combine_body<DK>(sm, blockIdx.x, dv, At, B, state);
+}
+
+// The combine of a split tail replay beside the suffix's chunk preparation,
+// one launch: blocks [0, n_comb) run k_state_combine, the rest k_intra for the
+// suffix chunks (with outputs).  The combine is short and light, so the
+// preparation workgroups fill the chip around it.  No workgroup waits for
+// another.
+template <typename TIn, int DK>
+__global__ __launch_bounds__(kCombineThreads)
+void k_combine_intra(int32_t n_comb, int32_t dv, const float* __restrict__ At, const float* __restrict__ B,
+                     float* __restrict__ state, int32_t slots_s, const int32_t* __restrict__ cu_s, int32_t num_seqs,
+                     int32_t hk, int32_t hv, const TIn* __restrict__ q_s, const TIn* __restrict__ k_s,
+                     const float* __restrict__ g_s, const float* __restrict__ beta_s, float scale,
+                     u32x4* __restrict__ Kw_s, u32x4* __restrict__ Tw_s, float* __restrict__ Sw_s,
+                     u32x4* __restrict__ Pw_s) {
+  static_assert(kCombineThreads == 4 * kWave, "the preparation body runs on four waves");
+  using LC = CombineLds<DK>;
+  using LI = IntraLds<TIn, DK, true>;
+  constexpr size_t kBytes = sizeof(LC) > sizeof(LI) ? sizeof(LC) : sizeof(LI);
+  __shared__ __attribute__((aligned(1024))) unsigned char smem[kBytes];
+  const int b = blockIdx.x;
+  if (b < n_comb) {
+    combine_body<DK>(*reinterpret_cast<LC*>(smem), b, dv, At, B, state);
+  } else {
+    const int i = b - n_comb;
+    intra_body<TIn, DK, true>(*reinterpret_cast<LI*>(smem), i % slots_s, i / slots_s, cu_s, num_seqs, hk, hv,
+                              q_s, k_s, g_s, beta_s, scale, Kw_s, Tw_s, Sw_s, Pw_s);
+  }
 }
 
 // ---------------------------------------------------------------- replay scan + suffix intra

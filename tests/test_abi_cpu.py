@@ -243,7 +243,8 @@ def test_replay_forward_workspace_is_both_plans():
                                                ctypes.cast(_cu(cs), ctypes.c_void_p), ctypes.byref(out))
     assert st == 0 and out.value == (nt + 255) // 256 * 256 + ns
     assert gdn.replay_forward_workspace_size(2, 16, 32, 128, 128, ct, cs) == out.value
-    assert gdn.replay_forward_stage_names() == ["tail intra", "tail scan + suffix intra", "suffix scan"]
+    assert gdn.replay_forward_stage_names() == ["tail intra", "tail scan (+ suffix intra)",
+                                                "combine (+ suffix intra)", "suffix scan"]
     assert gdn.stage_names(False) == ["intra", "scan", "combine"]
     assert gdn.stage_names(True) == ["intra", "scan"]
     assert lib.gdn_stage_name(0, 3) == b"" and lib.gdn_stage_name(1, 2) == b""

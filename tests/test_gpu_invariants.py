@@ -192,17 +192,27 @@ def test_whole_head_and_column_kernels_agree():
         assert rel.item() <= 1e-3   # bf16 outputs: one rounding step apart at most
 
 
-@pytest.mark.parametrize("case", ["one", "ragged", "wide", "ragged_d64", "ragged_dk64", "ragged_dv64"])
+@pytest.mark.parametrize("case", ["one", "ragged", "wide", "ragged_d64", "ragged_dk64", "ragged_dv64", "split",
+                                  "split_no_suffix"])
 def test_replay_forward_equals_the_two_calls_bitwise(case):
     # the fused call runs the same kernels (the suffix's chunk preparation
     # beside the tail scan), so it must reproduce tail_replay + chunk_forward
     # "ragged*" covers an empty tail and an empty suffix at every (d_k, d_v)
-    # the kernels are built for; "wide" runs the whole-head scan kernel
+    # the kernels are built for; "wide" runs the whole-head scan kernel;
+    # "split*": a 21-chunk tail at 32 heads, which both run in two halves (the
+    # fused call with the suffix's preparation beside the split scan, or with
+    # no suffix at all)
     shape = {"ragged_d64": synth.Shape(hk=2, hv=4, dk=64, dv=64, dtype="bf16"),
              "ragged_dk64": synth.Shape(hk=2, hv=4, dk=64, dv=128, dtype="bf16"),
-             "ragged_dv64": synth.Shape(hk=2, hv=4, dk=128, dv=64, dtype="bf16")}.get(case, SHAPE)
+             "ragged_dv64": synth.Shape(hk=2, hv=4, dk=128, dv=64, dtype="bf16"),
+             "split": synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16"),
+             "split_no_suffix": synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16")}.get(case, SHAPE)
     if case == "one":
         rs, ss = [333], [200]
+    elif case == "split":
+        rs, ss = [1300], [200]
+    elif case == "split_no_suffix":
+        rs, ss = [1300], [0]
     elif case.startswith("ragged"):
         rs, ss = [0, 1, 64, 130, 257], [65, 0, 1, 200, 64]
     else:   # enough heads that the whole-head scan kernel runs
@@ -226,9 +236,10 @@ def test_replay_forward_equals_the_two_calls_bitwise(case):
 @pytest.mark.parametrize("r,slow", [(1300, True), (1638, False), (2000, True), (3277, True), (3277, False)])
 def test_split_replay_agrees_with_one_chain(r, slow):
     """One sequence at 32 heads replays in two halves (the first half's state,
-    the second half's from zero and its transition, combined); the same
-    sequence in a batch of two exceeds the split grid and runs one chain, and
-    so does the fused call's tail.  The three differ by rounding order only.
+    the second half's from zero and its transition, combined), and so does the
+    fused call's tail (bit for bit); the same sequence in a batch of two
+    exceeds the split grid and runs one chain.  The two forms differ by
+    rounding order only.
     `slow`: gates that decay slowly (scale 0.002, beta x 0.1), so the first
     half's share of the state is large and the combine is exercised."""
     import dataclasses
@@ -246,12 +257,12 @@ def test_split_replay_agrees_with_one_chain(r, slow):
     _, mid, _ = gdn.replay_forward(x1["k"], x1["v"], x1["g"], x1["beta"], x1["cu"],
                                    xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"],
                                    cu_tail_host=x1["cu_host"], cu_suf_host=xs["cu_host"])
-    e_mid = state_err(to_f64(mid), to_f64(chain[:1]))
-    print(f"[split] r={r}: split vs one chain {e:.2e}, fused tail vs one chain {e_mid:.2e}", flush=True)
+    e_mid = state_err(to_f64(mid), to_f64(split))
+    print(f"[split] r={r}: split vs one chain {e:.2e}, fused tail vs split {e_mid:.2e}", flush=True)
     # each form is within ~5e-4 of the exact state (bf16 inputs: hi(T) alone in
     # T R), and the two round differently, so they differ by at most 1e-3
     assert e <= 1e-3
-    assert torch.equal(mid, chain[:1])
+    assert torch.equal(mid, split)
 
 
 def test_varlen_graph_with_longest_first_order():
