@@ -401,6 +401,16 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   }
 }
 
+// Logical (slot, value head) of intra workgroup i of n = slots x Hv: the
+// value heads of one key head read the same key rows, so they form one cluster
+// on one XCD (the second finds the rows in that XCD's L2), consecutive clusters
+// on consecutive XCDs.  A bijection, so correctness does not depend on it.
+__device__ __forceinline__ void intra_unit(int i, int n, int hv, int grp, int& slot, int& h) {
+  const int u = xcd_cluster_remap(i, n, grp);
+  slot = u / hv;
+  h = u % hv;
+}
+
 // grid = (num_slots, Hv): one workgroup per (chunk slot, value head).
 template <typename TIn, int DK, bool FWD>
 __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, int32_t num_seqs,
@@ -414,8 +424,9 @@ __global__ __launch_bounds__(256) void k_intra(const int32_t* __restrict__ cu, i
                                                float* __restrict__ Sw,
                                                u32x4* __restrict__ Pw) {
   __shared__ IntraLds<TIn, DK, FWD> sm;
-  intra_body<TIn, DK, FWD>(sm, blockIdx.x, blockIdx.y, cu, num_seqs, hk, hv, q, k, g, beta, scale, Kw, Tw,
-                           Sw, Pw);
+  int slot, h;
+  intra_unit(blockIdx.x + blockIdx.y * gridDim.x, gridDim.x * gridDim.y, hv, hv / hk, slot, h);
+  intra_body<TIn, DK, FWD>(sm, slot, h, cu, num_seqs, hk, hv, q, k, g, beta, scale, Kw, Tw, Sw, Pw);
 }
 
 }  // namespace gdn

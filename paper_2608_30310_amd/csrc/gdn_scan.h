@@ -966,17 +966,22 @@ struct CombineLds {
   alignas(16) float ms[DK * kCombineCols];
 };
 
+// `block` of `nblocks`: the column groups of one (sequence, head) are one
+// cluster on one XCD, so the head's transition is fetched from memory once
+// and its other workgroups find it in that XCD's L2.
 template <int DK>
-__device__ __forceinline__ void combine_body(CombineLds<DK>& sm, int block, int32_t dv, const float* __restrict__ At,
-                                             const float* __restrict__ B, float* __restrict__ state) {
+__device__ __forceinline__ void combine_body(CombineLds<DK>& sm, int block, int nblocks, int32_t dv,
+                                             const float* __restrict__ At, const float* __restrict__ B,
+                                             float* __restrict__ state) {
   constexpr int PER = DK * kCombineCols / kCombineThreads;   // staged column values per thread
   constexpr int AV = DK * DK / 4 / kCombineThreads;          // 16-byte pieces of A^T per thread
   constexpr int TILES = DK / 16 / (kCombineThreads / kWave);  // row tiles per wave
   float* as = sm.as;
   float* ms = sm.ms;
   const int groups = dv / kCombineCols;
-  const int64_t head = block / groups;
-  const int c0 = kCombineCols * (block % groups);
+  const int unit = xcd_cluster_remap(block, nblocks, groups);
+  const int64_t head = unit / groups;
+  const int c0 = kCombineCols * (unit % groups);
   const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
   const int li = lane % 16, lk = lane / 16;
   float* st = state + head * DK * dv + c0;
@@ -1021,7 +1026,7 @@ __global__ __launch_bounds__(kCombineThreads)
 void k_state_combine(int32_t dv, const float* __restrict__ At, const float* __restrict__ B,
                      float* __restrict__ state) {
   __shared__ CombineLds<DK> sm;
-  combine_body<DK>(sm, blockIdx.x, dv, At, B, state);
+  combine_body<DK>(sm, blockIdx.x, gridDim.x, dv, At, B, state);
 }
 
 // The combine of a split tail replay beside the suffix's chunk preparation,
@@ -1044,10 +1049,12 @@ void k_combine_intra(int32_t n_comb, int32_t dv, const float* __restrict__ At, c
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kBytes];
   const int b = blockIdx.x;
   if (b < n_comb) {
-    combine_body<DK>(*reinterpret_cast<LC*>(smem), b, dv, At, B, state);
+    combine_body<DK>(*reinterpret_cast<LC*>(smem), b, n_comb, dv, At, B, state);
   } else {
     const int i = b - n_comb;
-    intra_body<TIn, DK, true>(*reinterpret_cast<LI*>(smem), i % slots_s, i / slots_s, cu_s, num_seqs, hk, hv,
+    int slot, h;
+    intra_unit(i, slots_s * hv, hv, hv / hk, slot, h);
+    intra_body<TIn, DK, true>(*reinterpret_cast<LI*>(smem), slot, h, cu_s, num_seqs, hk, hv,
                               q_s, k_s, g_s, beta_s, scale, Kw_s, Tw_s, Sw_s, Pw_s);
   }
 }
@@ -1079,7 +1086,9 @@ void k_scan_cols_intra(int32_t n_scan, const int32_t* __restrict__ cu_t, int32_t
                                    Sw_t, nullptr, nullptr, nullptr, state_mid);
   } else {
     const int i = blockIdx.x - n_scan;
-    intra_body<TIn, DK, true>(*reinterpret_cast<LI*>(smem), i % slots_s, i / slots_s, cu_s, num_seqs, hk, hv,
+    int slot, h;
+    intra_unit(i, slots_s * hv, hv, hv / hk, slot, h);
+    intra_body<TIn, DK, true>(*reinterpret_cast<LI*>(smem), slot, h, cu_s, num_seqs, hk, hv,
                               q_s, k_s, g_s, beta_s, scale, Kw_s, Tw_s, Sw_s, Pw_s);
   }
 }
