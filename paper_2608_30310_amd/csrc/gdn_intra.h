@@ -62,26 +62,24 @@ struct IntraLds {
   static constexpr int KP = DK + 8;                 // padded LDS row (bf16 elements)
   static constexpr int NL = kSplit ? 2 : 1;         // hi (and lo) copies
   static constexpr int AP = kChunk + 4;             // fp32 row pitch of A, T and P
-  // The per-wave block scratch of the off-diagonal inverse steps takes the
-  // keys' place: the last key reads (the K record) end before those steps.
-  // Likewise P takes the queries' place: it stays in registers until the Q
-  // record is written.  And T = (I + A)^-1 is formed in A's place: every
-  // step of the inversion reads the blocks of A it needs before it writes the
-  // T block that replaces one of them, and never reads that A block again.
-  // Sizes (bf16, d_k = 128): tail replay 36 KiB, forward 53 KiB, three
-  // workgroups per CU either way (the register budget allows three).
+  // A takes the keys' place: every read of the key tile (the operands of
+  // K K^T and of the K record) is issued and waited for before the first
+  // element of A is written.  Likewise P takes the queries' place.  And
+  // T = (I + A)^-1 is formed in A's place: every step of the inversion reads
+  // the blocks of A it needs before it writes the T block that replaces one of
+  // them, and never reads that A block again.  Sizes (bf16, d_k = 128): tail
+  // replay 22 KiB (seven workgroups per CU), forward 39 KiB (four).
   union {
     alignas(16) uint16_t Ks[NL][kChunk][KP];
-    alignas(16) float Ys[4][16][17];
+    alignas(16) float As[kChunk][AP];               // A (strictly lower), then T = (I + A)^-1
   };
   union {
     alignas(16) uint16_t Qs[FWD ? NL : 1][FWD ? kChunk : 1][KP];
     alignas(16) float Ps[FWD ? kChunk : 1][AP];
   };
-  alignas(16) float As[kChunk][AP];                 // A (strictly lower), then T = (I + A)^-1
+  alignas(16) float Ys[4][16][17];                  // per-wave block scratch of the inverse steps
   alignas(16) float Gs[kChunk];
   alignas(16) float Bs[kChunk];
-  static_assert(sizeof(float[4][16][17]) <= sizeof(uint16_t[NL][kChunk][KP]), "block scratch fits in the keys");
 };
 
 // One intra workgroup for chunk slot `slot` and value head `h`, with its LDS
@@ -159,19 +157,30 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   __syncthreads();
 
   // ---- K K^T (and Q K^T) on MFMA, 10 lower tiles over 4 waves (tiles wave,
-  //      wave + 4, wave + 8), turned into A (and P).  All operand reads first,
-  //      then the MFMAs, then the elementwise pass.
+  //      wave + 4, wave + 8), and the K record of this key head (written by
+  //      the first value head of the group, waves 1..3).  Every read of the key
+  //      (and query) tile happens before the barrier below, since A (and P)
+  //      take their LDS afterwards; the MFMAs run before it too, so only the
+  //      accumulators and the record fragments wait in registers.
+  //      K record fragment f, lane (g, r), element j:
+  //        K   (ti, kk): K[16 ti + r][32 kk + kperm(g, j)]            f = ti * NK + kk
+  //        Q   (ti, kk): Q[16 ti + r][32 kk + kperm(g, j)]            f = NKA + ti * NK + kk
+  //      record layout [hi | lo][fragment][kslot(lane)]
   constexpr int TPW = 3;   // tiles of K K^T per wave, at most
-  f32x4 pkeep[TPW];        // this wave's tiles of P until the queries are dead
+  constexpr int PA = (NKA + 2) / 3;   // K record fragments per writer wave, per part
+  const bool writer = wave >= 1 && wave < kWork && h % grp == 0;
+  const int w3 = wave - 1;             // writer index 0..2
+  f32x4 acc[TPW], accq[TPW];
+  u32x4 va[NL][PA], vq[FWD ? NL : 1][FWD ? PA : 1];
+  auto tile_rc = [](int t, int& bi, int& bj) __attribute__((always_inline)) {
+    bi = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
+    bj = t - bi * (bi + 1) / 2;
+  };
   if (wave < kWork) {
-    Frag fa[TPW][NK], fb[TPW][NK], fq[TPW][NK];
-    f32x4 acc[TPW], accq[TPW];
-    auto tile_rc = [](int t, int& bi, int& bj) __attribute__((always_inline)) {
-      bi = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
-      bj = t - bi * (bi + 1) / 2;
-    };
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
+      acc[u] = zero4();
+      accq[u] = zero4();
       const int t = wave + 4 * u;
       if (t < 10) {
         int bi, bj;
@@ -179,36 +188,44 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
 #pragma unroll
         for (int kk = 0; kk < NK; ++kk) {
           const int c = 32 * kk + 8 * lg;
-          fa[u][kk].hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bi + lr][c]);
-          fb[u][kk].hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bj + lr][c]);
+          Frag fa, fb, fq;
+          fa.hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bi + lr][c]);
+          fb.hi = *reinterpret_cast<const bf16x8*>(&Ks[0][16 * bj + lr][c]);
           if constexpr (SPLIT) {
-            fa[u][kk].lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bi + lr][c]);
-            fb[u][kk].lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bj + lr][c]);
+            fa.lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bi + lr][c]);
+            fb.lo = *reinterpret_cast<const bf16x8*>(&Ks[NL - 1][16 * bj + lr][c]);
           }
           if constexpr (FWD) {
-            fq[u][kk].hi = *reinterpret_cast<const bf16x8*>(&Qs[0][16 * bi + lr][c]);
-            if constexpr (SPLIT) fq[u][kk].lo = *reinterpret_cast<const bf16x8*>(&Qs[NL - 1][16 * bi + lr][c]);
+            fq.hi = *reinterpret_cast<const bf16x8*>(&Qs[0][16 * bi + lr][c]);
+            if constexpr (SPLIT) fq.lo = *reinterpret_cast<const bf16x8*>(&Qs[NL - 1][16 * bi + lr][c]);
           }
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < TPW; ++u) {
-      acc[u] = zero4();
-      accq[u] = zero4();
-      if (wave + 4 * u < 10) {
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
           if constexpr (SPLIT) {
-            acc[u] = mma_x3(fa[u][kk], fb[u][kk], acc[u]);
-            if constexpr (FWD) accq[u] = mma_x3(fq[u][kk], fb[u][kk], accq[u]);
+            acc[u] = mma_x3(fa, fb, acc[u]);
+            if constexpr (FWD) accq[u] = mma_x3(fq, fb, accq[u]);
           } else {
-            acc[u] = mma(fa[u][kk].hi, fb[u][kk].hi, acc[u]);
-            if constexpr (FWD) accq[u] = mma(fq[u][kk].hi, fb[u][kk].hi, accq[u]);
+            acc[u] = mma(fa.hi, fb.hi, acc[u]);
+            if constexpr (FWD) accq[u] = mma(fq.hi, fb.hi, accq[u]);
           }
         }
       }
     }
+    if (writer) {
+      // fragment indices clamped so the reads are unconditional
+#pragma unroll
+      for (int p = 0; p < NL; ++p)
+#pragma unroll
+        for (int i = 0; i < PA; ++i) {
+          const int f = min(w3 + 3 * i, NKA - 1);
+          const int ti = f / NK, kk = f % NK;
+          va[p][i] = __builtin_bit_cast(u32x4, perm_frag(&Ks[p][16 * ti + lr][32 * kk + 4 * lg]));
+          if constexpr (FWD) vq[p][i] = __builtin_bit_cast(u32x4, perm_frag(&Qs[p][16 * ti + lr][32 * kk + 4 * lg]));
+        }
+    }
+  }
+  __syncthreads();   // the key and query tiles are dead from here
+
+  if (wave < kWork) {
+    // A (and P) from the accumulators
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
       const int t = wave + 4 * u;
@@ -224,7 +241,22 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
           const int i = 16 * bi + 4 * lg + r;
           const float decay = j <= i ? __expf(gi[r] - gj) : 0.f;
           As[i][j] = j < i ? bi4[r] * decay * acc[u][r] : 0.f;
-          if constexpr (FWD) pkeep[u][r] = scale * decay * accq[u][r];
+          if constexpr (FWD) Ps[i][j] = scale * decay * accq[u][r];
+        }
+      }
+    }
+    if (writer) {
+      u32x4* kdst = Kw + (static_cast<int64_t>(slot) * hk + kh) * (NL * NKF * kWave);
+#pragma unroll
+      for (int p = 0; p < NL; ++p) {
+        u32x4* pdst = kdst + static_cast<int64_t>(p) * NKF * kWave;
+#pragma unroll
+        for (int i = 0; i < PA; ++i) {
+          const int f = w3 + 3 * i;
+          if (f < NKA) {
+            pdst[f * kWave + kslot(lane)] = va[p][i];
+            if constexpr (FWD) pdst[(NKA + f) * kWave + kslot(lane)] = vq[p][i];
+          }
         }
       }
     }
@@ -252,61 +284,8 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
       for (int i = m + 1; i < 16; ++i) x[i] -= arow[i][m / 4][m % 4] * x[m];
 #pragma unroll
     for (int i = 0; i < 16; ++i) Ts[16 * b + i][16 * b + jj] = x[i];
-  } else if (wave < kWork && h % grp == 0) {
-    // ---- meanwhile, the K record of this key head: K (and Q) as bf16 A
-    //      operands (hi and lo parts for fp32 inputs).
-    //      fragment f, lane (g, r), element j:
-    //        K   (ti, kk): K[16 ti + r][32 kk + kperm(g, j)]            f = ti * NK + kk
-    //        Q   (ti, kk): Q[16 ti + r][32 kk + kperm(g, j)]            f = NKA + ti * NK + kk
-    //      record layout [hi | lo][fragment][kslot(lane)]
-    u32x4* kdst = Kw + (static_cast<int64_t>(slot) * hk + kh) * (NL * NKF * kWave);
-    // Three waves share each kind of fragment; every wave first reads all of its
-    // fragments (indices clamped so the reads are unconditional), then stores.
-    auto ka_val = [&](int p, int f) __attribute__((always_inline)) {   // f < NKA
-      const int ti = f / NK, kk = f % NK;
-      return __builtin_bit_cast(u32x4, perm_frag(&Ks[p][16 * ti + lr][32 * kk + 4 * lg]));
-    };
-    auto q_val = [&](int p, int f) __attribute__((always_inline)) {    // f < NKA
-      const int ti = f / NK, kk = f % NK;
-      return __builtin_bit_cast(
-          u32x4, perm_frag(&Qs[FWD ? p : 0][FWD ? 16 * ti + lr : 0][FWD ? 32 * kk + 4 * lg : 0]));
-    };
-    constexpr int PA = (NKA + 2) / 3;                        // per wave, per part
-    const int w3 = wave - 1;                                 // 0..2
-#pragma unroll
-    for (int p = 0; p < NL; ++p) {
-      u32x4* pdst = kdst + static_cast<int64_t>(p) * NKF * kWave;
-      u32x4 va[PA], vq[FWD ? PA : 1];
-#pragma unroll
-      for (int i = 0; i < PA; ++i) {
-        va[i] = ka_val(p, min(w3 + 3 * i, NKA - 1));
-        if constexpr (FWD) vq[i] = q_val(p, min(w3 + 3 * i, NKA - 1));
-      }
-#pragma unroll
-      for (int i = 0; i < PA; ++i) {
-        const int f = w3 + 3 * i;
-        if (f < NKA) {
-          pdst[f * kWave + kslot(lane)] = va[i];
-          if constexpr (FWD) pdst[(NKA + f) * kWave + kslot(lane)] = vq[i];
-        }
-      }
-    }
   }
   __syncthreads();
-
-  if (FWD && wave < kWork) {
-    // the Q record is written: P goes where the queries were
-#pragma unroll
-    for (int u = 0; u < TPW; ++u) {
-      const int t = wave + 4 * u;
-      if (t < 10) {
-        const int bi = t < 1 ? 0 : t < 3 ? 1 : t < 6 ? 2 : 3;
-        const int bj = t - bi * (bi + 1) / 2;
-#pragma unroll
-        for (int r = 0; r < 4; ++r) Ps[16 * bi + 4 * lg + r][16 * bj + lr] = pkeep[u][r];
-      }
-    }
-  }
 
   // ---- off-diagonal blocks by the block-inverse identity for a lower block
   //      triangular matrix: inv([[I + A11, 0], [A21, I + A22]]) has lower-left
