@@ -122,8 +122,8 @@ gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups, int* c
 // `marks` (tail replay only, may be NULL): the call whose stage events are
 // recorded; its combine stage starts before k_state_combine.
 template <typename TIn, int DK, int DV, bool FWD>
-gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, const void* v,
-                       const float* state_in, void* o, float* state_out, char* ws, hipStream_t stream,
+gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, const void* v, const void* k,
+                       const void* q, const float* state_in, void* o, float* state_out, char* ws, hipStream_t stream,
                        const Args* marks = nullptr, bool* combined = nullptr) {
   const u32x4* Kw = reinterpret_cast<const u32x4*>(ws + p.off_K);
   const u32x4* Tw = reinterpret_cast<const u32x4*>(ws + p.off_T);
@@ -142,8 +142,8 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
       float* a2 = reinterpret_cast<float*>(ws + p.off_A2);
       hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
                          dim3(cols_wide_threads()), 0, stream, static_cast<int32_t>(split_first_groups(s)), cu,
-                         s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw,
-                         state_out, m2, a2);
+                         s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
+                         static_cast<const TIn*>(q), Kw, Tw, Sw, state_out, m2, a2);
       if ((st = check_launch("split scan launch")) != GDN_OK) return st;
       if (marks && (st = mark(*marks, 2)) != GDN_OK) return st;
       if (combined) *combined = true;
@@ -155,18 +155,18 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
   }
   if (fits) {
     hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0, stream, cu,
-                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw, Pw,
-                       state_in, static_cast<TIn*>(o), state_out);
+                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
+                       static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o), state_out);
   } else if constexpr (kWide) {
     const uint32_t wide_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kColsWide);
     hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK>), dim3(wide_groups), dim3(cols_wide_threads()), 0, stream, cu,
-                       p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), Kw, Tw, Sw,
-                       state_out);
+                       p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
+                       static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, state_out);
   } else {
     hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
                        dim3(head_threads(DV)), 0, stream, cu, p.order, s.num_k_heads, s.num_v_heads,
-                       static_cast<const TIn*>(v), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o),
-                       state_out);
+                       static_cast<const TIn*>(v), static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw,
+                       Pw, state_in, static_cast<TIn*>(o), state_out);
   }
   return check_launch("scan launch");
 }
@@ -180,7 +180,8 @@ gdn_status run(const Args& a) {
     return st;
   if ((st = mark(a, 1)) != GDN_OK) return st;
   bool combined = false;
-  if ((st = launch_scan<TIn, DK, DV, FWD>(s, *a.p, a.cu, a.v, a.state_in, a.o, a.state_out, a.ws, a.stream,
+  if ((st = launch_scan<TIn, DK, DV, FWD>(s, *a.p, a.cu, a.v, a.k, a.q, a.state_in, a.o, a.state_out, a.ws,
+                                          a.stream,
                                           FWD ? nullptr : &a, &combined)) != GDN_OK)
     return st;
   if (!FWD && !combined) {
@@ -362,6 +363,7 @@ gdn_status run_fused(const FusedArgs& a) {
     hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
                        dim3(cols_wide_threads()), 0, a.stream, static_cast<int32_t>(split_first_groups(s)), a.cu_t,
                        s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v_t),
+                       static_cast<const TIn*>(a.k_t), static_cast<const TIn*>(nullptr),
                        reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
                        reinterpret_cast<const u32x4*>(a.ws_t + pt.off_T),
                        reinterpret_cast<const float*>(a.ws_t + pt.off_S), a.state_mid,
@@ -384,7 +386,8 @@ gdn_status run_fused(const FusedArgs& a) {
     const uint32_t blocks = n_scan + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
     hipLaunchKernelGGL((k_scan_cols_intra<TIn, DK>), dim3(blocks), dim3(4 * kWave), 0, a.stream,
                        static_cast<int32_t>(n_scan), a.cu_t, s.num_k_heads, s.num_v_heads, s.d_v,
-                       static_cast<const TIn*>(a.v_t), reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
+                       static_cast<const TIn*>(a.v_t), static_cast<const TIn*>(a.k_t),
+                       reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
                        reinterpret_cast<const u32x4*>(a.ws_t + pt.off_T),
                        reinterpret_cast<const float*>(a.ws_t + pt.off_S), a.state_mid,
                        static_cast<int32_t>(ps.num_slots), a.cu_s, s.num_seqs, static_cast<const TIn*>(a.q),
@@ -393,7 +396,8 @@ gdn_status run_fused(const FusedArgs& a) {
                        reinterpret_cast<float*>(a.ws_s + ps.off_S), reinterpret_cast<u32x4*>(a.ws_s + ps.off_P));
     if ((st = check_launch("tail scan + suffix intra launch")) != GDN_OK) return st;
   } else {
-    if ((st = launch_scan<TIn, DK, DV, false>(s, pt, a.cu_t, a.v_t, nullptr, nullptr, a.state_mid, a.ws_t,
+    if ((st = launch_scan<TIn, DK, DV, false>(s, pt, a.cu_t, a.v_t, a.k_t, nullptr, nullptr, nullptr, a.state_mid,
+                                              a.ws_t,
                                               a.stream)) != GDN_OK)
       return st;
     if ((st = launch_intra<TIn, DK, true>(s, ps, a.cu_s, a.q, a.k, a.g, a.beta, a.ws_s, a.stream)) != GDN_OK)
@@ -401,7 +405,7 @@ gdn_status run_fused(const FusedArgs& a) {
   }
   if (!combine && (st = fmark(a, 2)) != GDN_OK) return st;
   if ((st = fmark(a, 3)) != GDN_OK) return st;
-  if ((st = launch_scan<TIn, DK, DV, true>(s, ps, a.cu_s, a.v, a.state_mid, a.o, a.state_out, a.ws_s,
+  if ((st = launch_scan<TIn, DK, DV, true>(s, ps, a.cu_s, a.v, a.k, a.q, a.state_mid, a.o, a.state_out, a.ws_s,
                                            a.stream)) != GDN_OK)
     return st;
   return fmark(a, 4);

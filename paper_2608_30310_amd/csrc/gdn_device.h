@@ -155,6 +155,18 @@ __device__ __forceinline__ f32x4 mma_b(const Frag& a, const Frag& b, f32x4 c) {
 // + m of four quarters q at once) spread over twice as many bank groups as
 // without the rotation.
 __device__ __forceinline__ int kslot(int l) { return (l & 48) | ((l + 4 * (l >> 4)) & 15); }
+// The lane whose 16 bytes sit at position p (the inverse of kslot).
+__device__ __forceinline__ int kslot_inv(int p) { return (p & 48) | ((p + 16 - 4 * (p >> 4)) & 15); }
+
+// ---------------------------------------------------------------- state row order
+// The scan holds the state M (d_k x d_v) in MFMA accumulator tiles of 16 rows.
+// Lane (g, c) holds rows 4g..4g+3 of tile td, which are state rows
+// strow(td, g, 0..3): within each 32-row k step the tiles' rows are
+// interleaved so that the 8 rows a lane holds for a k step (tiles 2 kk and
+// 2 kk + 1) are the consecutive rows 32 kk + 8 g .. +7.  Then the contraction
+// slots of K M0 (and of (Q M0)^T) hit consecutive key (query) columns, and a
+// lane's operand is sixteen consecutive bytes of one key row.
+__device__ __forceinline__ int strow(int td, int g, int i) { return 32 * (td >> 1) + 8 * g + 4 * (td & 1) + i; }
 
 // ---------------------------------------------------------------- k-slot permutation
 // Within a 32-wide k step, MFMA slot 8g + j (g = lane/16, j = 0..7) is mapped to

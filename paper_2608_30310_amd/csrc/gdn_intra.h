@@ -157,18 +157,20 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
   __syncthreads();
 
   // ---- K K^T (and Q K^T) on MFMA, 10 lower tiles over 4 waves (tiles wave,
-  //      wave + 4, wave + 8), and the K record of this key head (written by
-  //      the first value head of the group, waves 1..3).  Every read of the key
-  //      (and query) tile happens before the barrier below, since A (and P)
-  //      take their LDS afterwards; the MFMAs run before it too, so only the
-  //      accumulators and the record fragments wait in registers.
+  //      wave + 4, wave + 8), and for fp32 inputs the K record of this key
+  //      head (written by the first value head of the group, waves 1..3; bf16
+  //      inputs need none: the scan fetches the key rows themselves).  Every
+  //      read of the key (and query) tile happens before the barrier below,
+  //      since A (and P) take their LDS afterwards; the MFMAs run before it
+  //      too, so only the accumulators and the record fragments wait in
+  //      registers.
   //      K record fragment f, lane (g, r), element j:
-  //        K   (ti, kk): K[16 ti + r][32 kk + kperm(g, j)]            f = ti * NK + kk
-  //        Q   (ti, kk): Q[16 ti + r][32 kk + kperm(g, j)]            f = NKA + ti * NK + kk
+  //        K   (ti, kk): K[16 ti + r][32 kk + 8 g + j]                f = ti * NK + kk
+  //        Q   (ti, kk): Q[16 ti + r][32 kk + 8 g + j]                f = NKA + ti * NK + kk
   //      record layout [hi | lo][fragment][kslot(lane)]
   constexpr int TPW = 3;   // tiles of K K^T per wave, at most
   constexpr int PA = (NKA + 2) / 3;   // K record fragments per writer wave, per part
-  const bool writer = wave >= 1 && wave < kWork && h % grp == 0;
+  const bool writer = SPLIT && wave >= 1 && wave < kWork && h % grp == 0;
   const int w3 = wave - 1;             // writer index 0..2
   f32x4 acc[TPW], accq[TPW];
   u32x4 va[NL][PA], vq[FWD ? NL : 1][FWD ? PA : 1];
@@ -217,8 +219,8 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
         for (int i = 0; i < PA; ++i) {
           const int f = min(w3 + 3 * i, NKA - 1);
           const int ti = f / NK, kk = f % NK;
-          va[p][i] = __builtin_bit_cast(u32x4, perm_frag(&Ks[p][16 * ti + lr][32 * kk + 4 * lg]));
-          if constexpr (FWD) vq[p][i] = __builtin_bit_cast(u32x4, perm_frag(&Qs[p][16 * ti + lr][32 * kk + 4 * lg]));
+          va[p][i] = *reinterpret_cast<const u32x4*>(&Ks[p][16 * ti + lr][32 * kk + 8 * lg]);
+          if constexpr (FWD) vq[p][i] = *reinterpret_cast<const u32x4*>(&Qs[p][16 * ti + lr][32 * kk + 8 * lg]);
         }
     }
   }

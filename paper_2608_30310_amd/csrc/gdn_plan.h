@@ -24,12 +24,15 @@ inline int64_t chunk_slot(int64_t seq_start, int64_t seq) { return seq_start / k
 // fragments and S the per-row scalars.  P is split into hi + lo parts; so is T
 // for fp32 inputs, while for bf16 inputs the scan multiplies by hi(T) alone
 // (the state's error stays below about 5e-4 relative, measured on the CPU with
-// a model of the kernels' rounding), so the record holds hi(T) only.  Per
-// (slot, key head), the K record holds the chunk's keys as A operands for K M
-// (4 row tiles x d_k/32 k steps) and, with outputs, the queries for Q M: one
-// bf16 part for bf16 inputs (exact), hi and lo parts for fp32 inputs.  The
-// scan takes the operands of K^T Delta from the same fragments with
-// transposing LDS reads.
+// a model of the kernels' rounding), so the record holds hi(T) only.  The
+// scan holds each chunk's keys in LDS as A operands for K M (4 row tiles x
+// d_k/32 k steps; lane (g, r) of fragment (ti, kk) holds K[16 ti + r][32 kk +
+// 8 g + j], j = 0..7, sixteen consecutive bytes of a key row) and, with
+// outputs, the queries in the same form for Q M; it takes the operands of K^T
+// Delta from the same fragments with transposing LDS reads.  For bf16 inputs
+// those fragments are the input rows themselves, fetched by the scan's DMA;
+// for fp32 inputs, which need hi and lo parts, the chunk preparation writes
+// them as a K record per (slot, key head).
 constexpr size_t kFragBytes = 1024;
 constexpr int kTFrags = 6;                                   // nonzero (row tile, k step) pairs
 constexpr size_t kPRecordBytes = 2 * kTFrags * kFragBytes;   // P, split hi/lo
@@ -41,8 +44,13 @@ constexpr int ka_frags(int dk) { return 4 * (dk / 32); }     // K as A for K M
 constexpr int k_record_frags(int dk, bool outputs) {          // per bf16 part
   return ka_frags(dk) + (outputs ? ka_frags(dk) : 0);
 }
-constexpr size_t k_record_bytes(int dk, bool outputs, bool split) {
+// the chunk's K (and Q) fragments in the scan's LDS
+constexpr size_t k_tile_bytes(int dk, bool outputs, bool split) {
   return static_cast<size_t>(k_record_frags(dk, outputs)) * (split ? 2 : 1) * kFragBytes;
+}
+// the K record in the workspace: fp32 inputs only
+constexpr size_t k_record_bytes(int dk, bool outputs, bool split) {
+  return split ? k_tile_bytes(dk, outputs, split) : 0;
 }
 
 // Longest-first order of a batch's sequences by chunk count (equal counts keep

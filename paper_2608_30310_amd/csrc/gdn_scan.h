@@ -98,15 +98,16 @@ __device__ __forceinline__ void store_out4(__amdgpu_buffer_rsrc_t r, int voff, c
 // P (outputs only) is staged in LDS when P_LDS, else read from global memory.
 template <typename TIn, int DK, int VC, bool FWD, bool P_LDS>
 struct ScanLds {
+  static constexpr int kDK = DK;
   static constexpr bool kSplit = sizeof(TIn) == 4;
   static constexpr bool kPInLds = FWD && P_LDS;
   static constexpr int kKFrags = k_record_frags(DK, FWD);         // per bf16 part
-  static constexpr int kKBytes = static_cast<int>(k_record_bytes(DK, FWD, kSplit));
+  static constexpr int kKBytes = static_cast<int>(k_tile_bytes(DK, FWD, kSplit));
   static constexpr int kTBytes = static_cast<int>(t_record_bytes(kSplit));
   static constexpr int kSBytes = static_cast<int>(kSRecordBytes);
   static constexpr int kVRowBytes = VC * static_cast<int>(sizeof(TIn));
   static constexpr int kVBytes = kChunk * kVRowBytes;
-  static constexpr int kOffK = 0;                 // K record
+  static constexpr int kOffK = 0;                 // K (and Q) fragments
   static constexpr int kOffT = kOffK + kKBytes;
   static constexpr int kPBytes = kPInLds ? static_cast<int>(kPRecordBytes) : 0;
   static constexpr int kOffP = kOffT + kTBytes;
@@ -114,8 +115,8 @@ struct ScanLds {
   static constexpr int kOffV = kOffS + 2048;      // S padded to two DMA blocks
   static constexpr int kBytes = kOffV + kVBytes;
   static constexpr int kBuffers = 2 * kBytes <= kLdsBytes ? 2 : 1;
-  // DMA jobs per chunk (one 1 KiB global_load_lds each): K record, T, P, V
-  // rows, then the scalars as one full and one quarter block
+  // DMA jobs per chunk (one 1 KiB global_load_lds each): K (and Q) fragments,
+  // T, P, V rows, then the scalars as one full and one quarter block
   static constexpr int kKJobs = kKBytes / 1024, kTJobs = kTBytes / 1024, kPJobs = kPBytes / 1024;
   static constexpr int kVJobs = kVBytes / 1024;
   static constexpr int kJobs = kKJobs + kTJobs + kPJobs + kVJobs + 2;
@@ -123,7 +124,10 @@ struct ScanLds {
 
 // Where one chunk's operands come from.
 struct ChunkSrc {
-  const unsigned char* krec;   // K record of (slot, key head)
+  const unsigned char* krec;   // K record of (slot, key head), fp32 inputs
+  const void* k0;              // key row 0 of the chunk (bf16 inputs: the fragments come from the rows)
+  const void* q0;              // query row 0 of the chunk (bf16 inputs, outputs only)
+  int64_t krow;                // elements between consecutive key (query) rows
   const unsigned char* trec;   // T record of (slot, value head)
   const unsigned char* prec;   // P record of (slot, value head), outputs only
   const unsigned char* srow;   // scalars of (slot, value head)
@@ -135,7 +139,20 @@ struct ChunkSrc {
 template <typename L, typename TIn>
 __device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, lds_byte* base, int j, int lane) {
   if (j < L::kKJobs) {
-    dma16(c.krec + 1024 * j + 16 * lane, base + L::kOffK + 1024 * j);
+    if constexpr (L::kSplit) {
+      dma16(c.krec + 1024 * j + 16 * lane, base + L::kOffK + 1024 * j);
+    } else {
+      // fragment j: keys for j < 4 d_k/32, then queries; the lane at position
+      // `lane` (kslot order) takes 16 bytes of row 16 ti + r at column 32 kk +
+      // 8 g; pad rows repeat the last row (their beta is 0, so they add nothing)
+      constexpr int NK = L::kDK / 32, NKA = ka_frags(L::kDK);
+      const bool isq = j >= NKA;
+      const int f = isq ? j - NKA : j;
+      const int l = kslot_inv(lane);
+      const int row = min(16 * (f / NK) + (l & 15), c.clen - 1);
+      const uint16_t* src = static_cast<const uint16_t*>(isq ? c.q0 : c.k0) + row * c.krow + 32 * (f % NK) + 8 * (l >> 4);
+      dma16(src, base + L::kOffK + 1024 * j);
+    }
   } else if (j < L::kKJobs + L::kTJobs) {
     const int t = j - L::kKJobs;
     dma16(c.trec + 1024 * t + 16 * lane, base + L::kOffT + 1024 * t);
@@ -447,12 +464,16 @@ __device__ __forceinline__ ScanUnit scan_unit(const int32_t* __restrict__ cu, in
 
 template <typename L, typename TIn>
 __device__ __forceinline__ ChunkSrc chunk_src(const ScanUnit& u, int ci, int hk, int hv, int dv, int col0,
-                                              const TIn* v, const u32x4* Kw, const u32x4* Tw,
-                                              const float* Sw, const u32x4* Pw) {
+                                              const TIn* v, const TIn* kin, const TIn* qin, const u32x4* Kw,
+                                              const u32x4* Tw, const float* Sw, const u32x4* Pw) {
   const int64_t srec = static_cast<int64_t>(u.slot0 + ci);
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
   ChunkSrc c;
   c.krec = reinterpret_cast<const unsigned char*>(Kw) + (srec * hk + u.kh) * L::kKBytes;
+  c.krow = static_cast<int64_t>(hk) * L::kDK;
+  const int64_t krow0 = static_cast<int64_t>(u.tok0 + ci * kChunk) * c.krow + static_cast<int64_t>(u.kh) * L::kDK;
+  c.k0 = kin + krow0;
+  c.q0 = qin ? qin + krow0 : nullptr;
   c.trec = reinterpret_cast<const unsigned char*>(Tw) + (srec * hv + u.h) * L::kTBytes;
   c.prec = reinterpret_cast<const unsigned char*>(Pw) + (srec * hv + u.h) * static_cast<int64_t>(kPRecordBytes);
   c.srow = reinterpret_cast<const unsigned char*>(Sw) + (srec * hv + u.h) * L::kSBytes;
@@ -469,7 +490,7 @@ __device__ __forceinline__ void load_state(const float* __restrict__ state_in, i
   for (int td = 0; td < DK / 16; ++td)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      M[td][r] = state_in ? state_in[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] : 0.f;
+      M[td][r] = state_in ? state_in[sbase + static_cast<int64_t>(strow(td, lg, r)) * dv] : 0.f;
 #pragma unroll
   for (int kk = 0; kk < DK / 32; ++kk) mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
 }
@@ -547,6 +568,7 @@ template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup, int PART = k
 __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int nblocks,
                                                const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                                int32_t dv, const TIn* __restrict__ v,
+                                               const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                                                const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                                                const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                const float* __restrict__ state_in, TIn* __restrict__ o,
@@ -590,7 +612,7 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
   const int col = col0 + 16 * wave + lr;
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
   auto dma_chunk = [&](int ci, int b) __attribute__((always_inline)) {
-    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, ident ? 0 : col0, v, Kw, Tw, Sw, Pw);
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, ident ? 0 : col0, v, kin, qin, Kw, Tw, Sw, Pw);
 #pragma unroll
     for (int j = 0; j < L::kJobs; ++j) {
       // the transition's value rows are the zeros written below
@@ -610,7 +632,7 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
 #pragma unroll
         for (int td = 0; td < NT; ++td)
 #pragma unroll
-          for (int r = 0; r < 4; ++r) M[td][r] = (16 * td + 4 * lg + r == col) ? 1.f : 0.f;
+          for (int r = 0; r < 4; ++r) M[td][r] = (strow(td, lg, r) == col) ? 1.f : 0.f;
 #pragma unroll
         for (int kk = 0; kk < DK / 32; ++kk) mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
       }
@@ -663,15 +685,15 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
     if (SPLIT && ident) {
       // the transition goes out transposed, A^T [d_k x d_k]: a lane's four
       // rows of column `col` are one 16-byte piece of row `col` of A^T
-      float* at = dst + ((static_cast<int64_t>(u.n) * hv + u.h) * DK + col) * DK + 4 * lg;
+      float* at = dst + ((static_cast<int64_t>(u.n) * hv + u.h) * DK + col) * DK;
 #pragma unroll
-      for (int td = 0; td < NT; ++td) *reinterpret_cast<f32x4*>(at + 16 * td) = M[td];
+      for (int td = 0; td < NT; ++td) *reinterpret_cast<f32x4*>(at + strow(td, lg, 0)) = M[td];
     } else if (dst) {
 #pragma unroll
       for (int td = 0; td < NT; ++td)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          dst[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * ld] = M[td][r];
+          dst[sbase + static_cast<int64_t>(strow(td, lg, r)) * ld] = M[td][r];
     }
   }
 }
@@ -710,6 +732,7 @@ template <typename TIn, int DK>
 __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, int nblocks,
                                                    const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                                    int32_t dv, const TIn* __restrict__ v,
+                                                   const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                                                    const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                                                    const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                    const float* __restrict__ state_in, TIn* __restrict__ o,
@@ -749,7 +772,7 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   // compile-time constant in each instance, so every job is straight code)
   auto dma_jobs = [&](int ci, int b, auto j0c, auto j1c) __attribute__((always_inline)) {
     constexpr int j0 = decltype(j0c)::value, j1 = decltype(j1c)::value;
-    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, kin, qin, Kw, Tw, Sw, Pw);
 #pragma unroll
     for (int j = j0; j < j1; ++j) dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
   };
@@ -761,7 +784,7 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   // record a job reads is known at compile time); the scalars with the
   // second half
   auto dma_half = [&](int ci, int b, int q0, int q1) __attribute__((always_inline)) {
-    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, Kw, Tw, Sw, Pw);
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, col0, v, kin, qin, Kw, Tw, Sw, Pw);
     lds_byte* dst = lds_l + b * L::kBytes;
 #pragma unroll
     for (int q = q0; q < q1; ++q) {
@@ -889,24 +912,25 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
     for (int td = 0; td < NT; ++td)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * dv] = M[td][r];
+        state_out[sbase + static_cast<int64_t>(strow(td, lg, r)) * dv] = M[td][r];
   }
 }
 
 template <typename TIn, int DK, bool FWD>
 __global__ __launch_bounds__(cols_threads(FWD, sizeof(TIn) == 4)) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
-                 const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                 const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
+                 const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                  const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                  const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
   if constexpr (FWD) {
     __shared__ __attribute__((aligned(1024))) unsigned char lds[ColsOutLayout<TIn, DK>::kBytes];
-    scan_cols_out_body<TIn, DK>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw, Sw, Pw,
+    scan_cols_out_body<TIn, DK>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin, Kw, Tw, Sw, Pw,
                                 state_in, o, state_out);
   } else {
     using L = ColsLds<TIn, DK, false>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
-    scan_cols_body<TIn, DK, false>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw, Sw, Pw,
+    scan_cols_body<TIn, DK, false>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin, Kw, Tw, Sw, Pw,
                                    state_in, o, state_out);
   }
 }
@@ -915,11 +939,13 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
 template <typename TIn, int DK>
 __global__ __launch_bounds__(cols_wide_threads())
 void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
-                      const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                      const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
+                 const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                       const float* __restrict__ Sw, float* __restrict__ state_out) {
   using L = ColsLds<TIn, DK, false, kColsWide>;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
-  scan_cols_body<TIn, DK, false, kColsWide>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, Kw, Tw,
+  scan_cols_body<TIn, DK, false, kColsWide>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin,
+                                            Kw, Tw,
                                             Sw, nullptr, nullptr, nullptr, state_out, SplitOut{}, &order);
 }
 
@@ -931,7 +957,8 @@ void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int3
 template <typename TIn, int DK>
 __global__ __launch_bounds__(cols_wide_threads())
 void k_scan_cols_split(int32_t n_first, const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
-                       const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                       const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
+                       const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                        const float* __restrict__ Sw, float* __restrict__ state_out, float* __restrict__ m2,
                        float* __restrict__ a2) {
   using L1 = ColsLds<TIn, DK, false, kColsPerGroup>;
@@ -941,11 +968,12 @@ void k_scan_cols_split(int32_t n_first, const int32_t* __restrict__ cu, int32_t 
   const int b = blockIdx.x;
   if (b < n_first)
     scan_cols_body<TIn, DK, false, kColsPerGroup, kFirstHalf>((lds_byte*)lds, b, n_first, cu, hk, hv, dv, v,
-                                                              Kw, Tw, Sw, nullptr, nullptr, nullptr, state_out);
+                                                              kin, qin, Kw, Tw, Sw, nullptr, nullptr, nullptr,
+                                                              state_out);
   else
     scan_cols_body<TIn, DK, false, kColsWide, kSecondHalf>((lds_byte*)lds, b - n_first,
                                                            static_cast<int>(gridDim.x) - n_first, cu, hk, hv,
-                                                           dv, v, Kw, Tw, Sw, nullptr, nullptr, nullptr,
+                                                           dv, v, kin, qin, Kw, Tw, Sw, nullptr, nullptr, nullptr,
                                                            nullptr, SplitOut{m2, a2});
 }
 
@@ -1068,7 +1096,7 @@ void k_combine_intra(int32_t n_comb, int32_t dv, const float* __restrict__ At, c
 template <typename TIn, int DK>
 __global__ __launch_bounds__(4 * kWave) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_scan_cols_intra(int32_t n_scan, const int32_t* __restrict__ cu_t, int32_t hk, int32_t hv, int32_t dv,
-                       const TIn* __restrict__ v_t, const u32x4* __restrict__ Kw_t,
+                       const TIn* __restrict__ v_t, const TIn* __restrict__ k_t, const u32x4* __restrict__ Kw_t,
                        const u32x4* __restrict__ Tw_t, const float* __restrict__ Sw_t,
                        float* __restrict__ state_mid,
                        int32_t slots_s, const int32_t* __restrict__ cu_s, int32_t num_seqs,
@@ -1082,7 +1110,8 @@ void k_scan_cols_intra(int32_t n_scan, const int32_t* __restrict__ cu_t, int32_t
   constexpr size_t kBytes = kScanBytes > sizeof(LI) ? kScanBytes : sizeof(LI);
   __shared__ __attribute__((aligned(1024))) unsigned char smem[kBytes];
   if (static_cast<int>(blockIdx.x) < n_scan) {
-    scan_cols_body<TIn, DK, false>((lds_byte*)smem, blockIdx.x, n_scan, cu_t, hk, hv, dv, v_t, Kw_t, Tw_t,
+    scan_cols_body<TIn, DK, false>((lds_byte*)smem, blockIdx.x, n_scan, cu_t, hk, hv, dv, v_t, k_t, nullptr, Kw_t,
+                                   Tw_t,
                                    Sw_t, nullptr, nullptr, nullptr, state_mid);
   } else {
     const int i = blockIdx.x - n_scan;
@@ -1103,7 +1132,8 @@ constexpr int head_threads(int dv) { return dv / 16 * kWave; }
 template <typename TIn, int DK, int DV, bool FWD>
 __global__ __launch_bounds__(head_threads(DV))
 void k_scan_head(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv,
-                 const TIn* __restrict__ v, const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                 const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
+                 const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                  const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                  const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
   using L = ScanLds<TIn, DK, DV, FWD, false>;
@@ -1122,7 +1152,7 @@ void k_scan_head(const int32_t* __restrict__ cu, const SeqOrder order, int32_t h
   const int64_t vrow = static_cast<int64_t>(hv) * DV;
   // jobs wave + W * jj, jj in [j0, j1), of chunk ci into buffer b
   auto dma_share = [&](int ci, int b, int j0, int j1) __attribute__((always_inline)) {
-    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, DV, 0, v, Kw, Tw, Sw, Pw);
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, DV, 0, v, kin, qin, Kw, Tw, Sw, Pw);
 #pragma unroll
     for (int jj = j0; jj < j1; ++jj) {
       const int j = wave + W * jj;
@@ -1172,7 +1202,7 @@ void k_scan_head(const int32_t* __restrict__ cu, const SeqOrder order, int32_t h
     for (int td = 0; td < NT; ++td)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        state_out[sbase + static_cast<int64_t>(16 * td + 4 * lg + r) * DV] = M[td][r];
+        state_out[sbase + static_cast<int64_t>(strow(td, lg, r)) * DV] = M[td][r];
   }
 }
 

@@ -90,14 +90,15 @@ def test_workspace_size_null_args():
 def test_workspace_size_values():
     # 819 tokens -> 13 chunk slots.  Per (slot, value head): T as 6 fragments,
     # hi only for bf16 inputs (6 KiB; hi and lo for fp32, 12 KiB) + 5 rows of
-    # 64 fp32 scalars; outputs add P, split (12 KiB).  Per (slot, key head):
-    # the K record, K [and Q] as 4 x d_k / 32 1 KiB fragments each, one bf16
-    # part for bf16 inputs, hi and lo for fp32.
+    # 64 fp32 scalars; outputs add P, split (12 KiB).  Per (slot, key head),
+    # fp32 inputs only: the K record, K [and Q] as 4 x d_k / 32 1 KiB
+    # fragments each, hi and lo parts (the scan fetches bf16 key and query
+    # rows themselves).
     t_rec, s_rec, frag = 6 * 1024, 5 * 64 * 4, 1024
     p_rec = 6 * 2 * 1024
 
     def krec(dk=128, outputs=False, split=False):
-        return 4 * (dk // 32) * (2 if outputs else 1) * (2 if split else 1) * frag
+        return 4 * (dk // 32) * (2 if outputs else 1) * 2 * frag if split else 0
 
     records = 13 * 32 * (t_rec + s_rec) + 13 * 16 * krec()
     st, n = _ws_size(_shape(), _cu([0, 819]))
