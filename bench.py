@@ -72,6 +72,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true", help="time eager launches only")
     ap.add_argument("--no-workload1", action="store_true", help="skip the one-layer workload's extra keys")
+    ap.add_argument("--no-batched", action="store_true",
+                    help="skip the batched form (counter runs: only the per-layer launches)")
     ap.add_argument("--cold-reps", type=int, default=10,
                     help="rebuilds of the stack timed after an Infinity Cache flush")
     ap.add_argument("--calib-copy", action="store_true",
@@ -179,7 +181,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path=None, workload=None):
     f_write = CALIB_BYTES / (cal_write * 1024.0)
     kernels = {}
     for name in fetch:
-        if not any(t in name for t in ("k_scan", "k_intra", "k_decode", "k_state_combine")):
+        if not any(t in name for t in ("k_scan", "k_intra", "k_decode", "k_state_combine", "k_combine_intra")):
             continue
         short = name.split("(")[0].replace("void ", "")
         fb = fetch[name] * 1024.0 * f_fetch
@@ -195,7 +197,7 @@ def summarize_pmc(fetch_dir, write_dir, out_path=None, workload=None):
                "commands": [
                    "cd /tmp && export TMPDIR=/tmp && timeout -s KILL 120 rocprofv3 --pmc FETCH_SIZE "
                    "--output-format csv -d $OUT/pmc_fetch -o fetch -- python3 $ROOT/bench.py "
-                   "--no-cpu-baseline --no-graph --no-workload1 --steps 5 --warmup 2 --cold-reps 0 --calib-copy",
+                   "--no-cpu-baseline --no-graph --no-workload1 --steps 5 --warmup 2 --cold-reps 0 --calib-copy --no-batched",
                    "(same with WRITE_SIZE into $OUT/pmc_write)",
                    f"python bench.py --summarize-pmc $OUT/pmc_fetch $OUT/pmc_write"]}
     path = out_path or TRAFFIC_FILE
@@ -360,7 +362,8 @@ def main():
 
     for _ in range(args.warmup):
         step()
-        batched_step()
+        if not args.no_batched:
+            batched_step()
     torch.cuda.synchronize()
     K = args.steps
 
@@ -406,15 +409,17 @@ def main():
     two_calls_step()
     torch.cuda.synchronize()
     two_calls_equal = bool(torch.equal(mid, want[0]) and torch.equal(fin, want[1]) and torch.equal(o, want[2]))
-    batched_step()
-    torch.cuda.synchronize()
-    bdiff = float(((finb - want[1]).norm() / want[1].norm()).item())
+    bdiff = None
+    if not args.no_batched:
+        batched_step()
+        torch.cuda.synchronize()
+        bdiff = float(((finb - want[1]).norm() / want[1].norm()).item())
 
     ms_per_step = timed(step)
     ms_graph = timed(graph.replay) if graph is not None else None
     ms_two_calls = timed(two_calls_step)
-    ms_batched = timed(batched_step)
-    ms_batched_rebuild = timed(batched_replay)
+    ms_batched = None if args.no_batched else timed(batched_step)
+    ms_batched_rebuild = None if args.no_batched else timed(batched_replay)
 
     # ---- per-stage kernel durations: events recorded by the library on its stream
     n_ev = min(K, 20)
@@ -543,9 +548,9 @@ def main():
         "rebuild_latency_warm_us": warm,
         "rebuild_latency_cold_us": cold,
         "rebuild_latency_queued_us": queued_rebuild,
-        "rebuild_latency_batched_us": ms_batched_rebuild * 1e3,
+        "rebuild_latency_batched_us": None if ms_batched_rebuild is None else ms_batched_rebuild * 1e3,
         "replay_tokens_per_s": L * r / (warm["p50"] * 1e-6),
-        "replay_tokens_per_s_batched": L * r / (ms_batched_rebuild * 1e-3),
+        "replay_tokens_per_s_batched": None if ms_batched_rebuild is None else L * r / (ms_batched_rebuild * 1e-3),
         "stages": stages,
         "path": {"flops": path_flops, "bytes": path_bytes, "roofline_us": path_bound_s * 1e6,
                  "roofline_frac": path_bound_s / t_s,
