@@ -105,9 +105,10 @@ gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, co
 // The column-split scan has the shortest chunk latency but one workgroup per
 // CU; it is used when its grid fits on the chip at once.  Tail replay of bf16
 // inputs whose split grid (the two halves of the chain side by side and the
-// second half's transition) also fits runs split, which halves the chain.  When the 32-wide grid does not fit, tail replay of bf16 inputs takes
-// the 64-wide column scan (the same chunk latency, twice the columns per CU)
-// and everything else the whole-head scan.
+// second half's transition) also fits runs split, which halves the chain.
+// When the 32-wide grid does not fit, tail replay of bf16 inputs takes the
+// wide column scan (two tiles per wave, two workgroups per CU: throughput) and
+// everything else the whole-head scan.
 gdn_status cols_fit(const gdn_shape& s, bool* fits, uint32_t* col_groups, int* cus_out = nullptr) {
   int dev = 0, cus = 0;
   if (hipGetDevice(&dev) != hipSuccess ||
@@ -141,8 +142,8 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
       float* m2 = reinterpret_cast<float*>(ws + p.off_M2);
       float* a2 = reinterpret_cast<float*>(ws + p.off_A2);
       hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
-                         dim3(cols_wide_threads()), 0, stream, static_cast<int32_t>(split_first_groups(s)), cu,
-                         s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
+                         dim3(cols_split_threads()), 0, stream,
+                         static_cast<int32_t>(split_first_groups(s)), cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
                          static_cast<const TIn*>(q), Kw, Tw, Sw, state_out, m2, a2);
       if ((st = check_launch("split scan launch")) != GDN_OK) return st;
       if (marks && (st = mark(*marks, 2)) != GDN_OK) return st;
@@ -158,9 +159,11 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
                        s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
                        static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o), state_out);
   } else if constexpr (kWide) {
-    const uint32_t wide_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kColsWide);
-    hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK>), dim3(wide_groups), dim3(cols_wide_threads()), 0, stream, cu,
-                       p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
+    // a whole head per workgroup (128 columns, four compute waves) where d_v allows
+    constexpr int kCols = DV >= 128 ? 128 : 64;
+    const uint32_t wide_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCols);
+    hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK, kCols>), dim3(wide_groups), dim3(cols_wide_threads(kCols)), 0,
+                       stream, cu, p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
                        static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, state_out);
   } else {
     hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
@@ -357,31 +360,34 @@ gdn_status run_fused(const FusedArgs& a) {
   if ((st = cols_fit(s, &fits, &n_scan, &cus)) != GDN_OK) return st;
   constexpr bool kCanSplit = sizeof(TIn) == 2;   // the split form is bf16 tail replay
   bool combine = false;
-  if (kCanSplit && pt.split && split_groups(s) <= cus && ps.num_slots > 0) {
-    // the tail in two halves (as gdn_tail_replay runs it), then its combine
-    // with the suffix's records built beside it
-    hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
-                       dim3(cols_wide_threads()), 0, a.stream, static_cast<int32_t>(split_first_groups(s)), a.cu_t,
-                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v_t),
-                       static_cast<const TIn*>(a.k_t), static_cast<const TIn*>(nullptr),
-                       reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
-                       reinterpret_cast<const u32x4*>(a.ws_t + pt.off_T),
-                       reinterpret_cast<const float*>(a.ws_t + pt.off_S), a.state_mid,
-                       reinterpret_cast<float*>(a.ws_t + pt.off_M2), reinterpret_cast<float*>(a.ws_t + pt.off_A2));
-    if ((st = check_launch("split scan launch")) != GDN_OK) return st;
-    if ((st = fmark(a, 2)) != GDN_OK) return st;
-    const uint32_t n_comb = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCombineCols);
-    const uint32_t blocks = n_comb + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
-    hipLaunchKernelGGL((k_combine_intra<TIn, DK>), dim3(blocks), dim3(kCombineThreads), 0, a.stream,
-                       static_cast<int32_t>(n_comb), s.d_v, reinterpret_cast<const float*>(a.ws_t + pt.off_A2),
-                       reinterpret_cast<const float*>(a.ws_t + pt.off_M2), a.state_mid,
-                       static_cast<int32_t>(ps.num_slots), a.cu_s, s.num_seqs, s.num_k_heads, s.num_v_heads,
-                       static_cast<const TIn*>(a.q), static_cast<const TIn*>(a.k), a.g, a.beta, s.scale,
-                       reinterpret_cast<u32x4*>(a.ws_s + ps.off_K), reinterpret_cast<u32x4*>(a.ws_s + ps.off_T),
-                       reinterpret_cast<float*>(a.ws_s + ps.off_S), reinterpret_cast<u32x4*>(a.ws_s + ps.off_P));
-    if ((st = check_launch("combine + suffix intra launch")) != GDN_OK) return st;
-    combine = true;
-  } else if (fits && ps.num_slots > 0) {
+  if constexpr (kCanSplit) {
+    if (pt.split && split_groups(s) <= cus && ps.num_slots > 0) {
+      // the tail in two halves (as gdn_tail_replay runs it), then its combine
+      // with the suffix's records built beside it
+      hipLaunchKernelGGL((k_scan_cols_split<TIn, DK>), dim3(static_cast<uint32_t>(split_groups(s))),
+                         dim3(cols_split_threads()), 0, a.stream,
+                         static_cast<int32_t>(split_first_groups(s)), a.cu_t, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(a.v_t),
+                         static_cast<const TIn*>(a.k_t), static_cast<const TIn*>(nullptr),
+                         reinterpret_cast<const u32x4*>(a.ws_t + pt.off_K),
+                         reinterpret_cast<const u32x4*>(a.ws_t + pt.off_T),
+                         reinterpret_cast<const float*>(a.ws_t + pt.off_S), a.state_mid,
+                         reinterpret_cast<float*>(a.ws_t + pt.off_M2), reinterpret_cast<float*>(a.ws_t + pt.off_A2));
+      if ((st = check_launch("split scan launch")) != GDN_OK) return st;
+      if ((st = fmark(a, 2)) != GDN_OK) return st;
+      const uint32_t n_comb = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCombineCols);
+      const uint32_t blocks = n_comb + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
+      hipLaunchKernelGGL((k_combine_intra<TIn, DK>), dim3(blocks), dim3(kCombineThreads), 0, a.stream,
+                         static_cast<int32_t>(n_comb), s.d_v, reinterpret_cast<const float*>(a.ws_t + pt.off_A2),
+                         reinterpret_cast<const float*>(a.ws_t + pt.off_M2), a.state_mid,
+                         static_cast<int32_t>(ps.num_slots), a.cu_s, s.num_seqs, s.num_k_heads, s.num_v_heads,
+                         static_cast<const TIn*>(a.q), static_cast<const TIn*>(a.k), a.g, a.beta, s.scale,
+                         reinterpret_cast<u32x4*>(a.ws_s + ps.off_K), reinterpret_cast<u32x4*>(a.ws_s + ps.off_T),
+                         reinterpret_cast<float*>(a.ws_s + ps.off_S), reinterpret_cast<u32x4*>(a.ws_s + ps.off_P));
+      if ((st = check_launch("combine + suffix intra launch")) != GDN_OK) return st;
+      combine = true;
+    }
+  }
+  if (!combine && fits && ps.num_slots > 0) {
     // the suffix's records are built on the CUs the tail replay leaves idle
     const uint32_t blocks = n_scan + static_cast<uint32_t>(ps.num_slots) * s.num_v_heads;
     hipLaunchKernelGGL((k_scan_cols_intra<TIn, DK>), dim3(blocks), dim3(4 * kWave), 0, a.stream,
@@ -395,7 +401,7 @@ gdn_status run_fused(const FusedArgs& a) {
                        reinterpret_cast<u32x4*>(a.ws_s + ps.off_K), reinterpret_cast<u32x4*>(a.ws_s + ps.off_T),
                        reinterpret_cast<float*>(a.ws_s + ps.off_S), reinterpret_cast<u32x4*>(a.ws_s + ps.off_P));
     if ((st = check_launch("tail scan + suffix intra launch")) != GDN_OK) return st;
-  } else {
+  } else if (!combine) {
     if ((st = launch_scan<TIn, DK, DV, false>(s, pt, a.cu_t, a.v_t, a.k_t, nullptr, nullptr, nullptr, a.state_mid,
                                               a.ws_t,
                                               a.stream)) != GDN_OK)

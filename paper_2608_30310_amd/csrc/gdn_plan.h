@@ -98,11 +98,14 @@ struct Plan {
 constexpr int64_t kSplitMaxGroups = 256;
 
 constexpr int32_t kSplitMinChunks = 20;
+// state columns per workgroup of the first and of the second half
+constexpr int kSplitCols1 = 32, kSplitCols2 = 64;
 inline int64_t split_first_groups(const gdn_shape& s) {
-  return static_cast<int64_t>(s.num_seqs) * s.num_v_heads * (s.d_v / 32);
+  return static_cast<int64_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kSplitCols1);
 }
 inline int64_t split_groups(const gdn_shape& s) {
-  return split_first_groups(s) + static_cast<int64_t>(s.num_seqs) * s.num_v_heads * ((s.d_v + s.d_k) / 64);
+  return split_first_groups(s) +
+         static_cast<int64_t>(s.num_seqs) * s.num_v_heads * ((s.d_v + s.d_k) / kSplitCols2);
 }
 
 // ---------------------------------------------------------------- layer block

@@ -264,7 +264,7 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
   Frag ka0[2][NK], qa0[2][NK], ka1[2][NK], qa1[2][NK];
   Frag tfr[kTFrags];
   Frag kt0[NT], kt1[NT];
-  f32x4 km[4], qm[4], acc[NT], bv[4], R[4], D[4];
+  f32x4 km[4], qm[4], bv[4], R[4], D[4];
   u32x2 vraw[4];
   float vf[4][4];
 
@@ -393,8 +393,8 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
 #pragma unroll
   for (int td = 0; td < NT; ++td) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) acc[td][r] = eg * M[td][r];
-    acc[td] = mma_a<SPLIT>(kt0[td], db0, acc[td]);
+    for (int r = 0; r < 4; ++r) M[td][r] *= eg;
+    M[td] = mma_a<SPLIT>(kt0[td], db0, M[td]);
   }
   make_dw(2);
   make_dw(3);
@@ -425,8 +425,8 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
   // ---- region 6: M1, k step 1 (tokens 32..63) | split of M1 for the next chunk
 #pragma unroll
   for (int kk = 0; kk < NK; ++kk) {
-    M[2 * kk] = mma_a<SPLIT>(kt1[2 * kk], db1, acc[2 * kk]);
-    M[2 * kk + 1] = mma_a<SPLIT>(kt1[2 * kk + 1], db1, acc[2 * kk + 1]);
+    M[2 * kk] = mma_a<SPLIT>(kt1[2 * kk], db1, M[2 * kk]);
+    M[2 * kk + 1] = mma_a<SPLIT>(kt1[2 * kk + 1], db1, M[2 * kk + 1]);
     mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
   }
   if constexpr (EXPORT) {
@@ -437,6 +437,165 @@ __device__ __forceinline__ void chunk_step(const unsigned char* base, int vc0, c
       x[(2 * kk + 1) * kWave + lane] = __builtin_bit_cast(u32x4, mb[kk].lo);
     }
   }
+}
+
+// One 64-token chunk of tail replay (no outputs, bf16 inputs) for a wave that
+// carries NC tiles of 16 state columns: the products of chunk_step in the same
+// order with the same roundings (so the state is bit for bit that of NC waves
+// of one tile each), but every operand that does not depend on the state (K,
+// T, K^T) is read from LDS once for all NC tiles, and K M0 runs k step by k
+// step (the four row tiles' K fragments of one step, shared by the tiles), so
+// only two steps' operands are held at a time.  The tiles' chains are
+// independent, so each phase has NC times the MFMAs to cover the LDS reads
+// issued for the next.  hook(p) runs at the start of phase p, p = 0 ..
+// tiles_phases(DK) - 1 (a workgroup without a DMA wave issues the next
+// chunk's DMA there).
+constexpr int tiles_phases(int dk) { return dk / 32 + 6; }
+template <typename L, int DK, int NC, typename Hook>
+__device__ __forceinline__ void chunk_step_tiles(const unsigned char* base, int vc0, int lane,
+                                                 f32x4 (&M)[NC][DK / 16], Frag (&mb)[NC][DK / 32],
+                                                 Hook&& hook) {
+  static_assert(!L::kSplit, "bf16 inputs: K, K^T and hi(T) are single bf16 operands");
+  constexpr int NT = DK / 16, NK = DK / 32;
+  constexpr int VRB = L::kVRowBytes;
+  const int lg = lane / 16, lr = lane % 16;
+  const u32x4* kf = reinterpret_cast<const u32x4*>(base + L::kOffK);
+  const u32x4* tf = reinterpret_cast<const u32x4*>(base + L::kOffT);
+  const float* sc = reinterpret_cast<const float*>(base + L::kOffS);
+  const unsigned char* vtile = base + L::kOffV;
+  const int klane = kslot(lane);
+  // K fragment of row tile ti, k step kk (lanes in kslot order)
+  auto ldk = [&](int ti, int kk) __attribute__((always_inline)) {
+    return __builtin_bit_cast(bf16x8, kf[(ti * NK + kk) * kWave + klane]);
+  };
+  // K^T operand of row tile td of M for token k step kk (as in chunk_step)
+  const int kt_off = 16 * kslot(16 * (lr % 4) + 4 * lg + lr / 4);
+  auto ldkt = [&](int td, int kk) __attribute__((always_inline)) {
+    const unsigned char* f0 = reinterpret_cast<const unsigned char*>(kf + ((2 * kk) * NK + td / 2) * kWave);
+    const unsigned char* f1 = reinterpret_cast<const unsigned char*>(kf + ((2 * kk + 1) * NK + td / 2) * kWave);
+    const int o = kt_off + 8 * (td % 2);
+    return __builtin_bit_cast(bf16x8, join_halves(lds_read_tr16(f0 + o), lds_read_tr16(f1 + o)));
+  };
+
+  // ---- V (transposing reads: lane (g, c) gets V[16 ti + 4 g + r][c]) and the
+  //      first k step's K
+  hook(0);
+  u32x2 vraw[NC][4];
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti)
+      vraw[c][ti] = lds_read_tr16(vtile + swz<VRB>(16 * ti + 4 * lg + lr / 4, 2 * (vc0 + 16 * c + 4 * (lr % 4))));
+  bf16x8 ka[2][4];
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti) ka[0][ti] = ldk(ti, 0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- K M0, one k step at a time; the next step's K (after the last, T) arrives
+  f32x4 km[NC][4];
+  bf16x8 tfr[kTFrags];
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk) {
+    hook(1 + kk);
+    if (kk + 1 < NK) {
+#pragma unroll
+      for (int ti = 0; ti < 4; ++ti) ka[(kk + 1) & 1][ti] = ldk(ti, kk + 1);
+    } else {
+#pragma unroll
+      for (int f = 0; f < kTFrags; ++f) tfr[f] = __builtin_bit_cast(bf16x8, tf[f * kWave + lane]);
+    }
+#pragma unroll
+    for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        km[c][ti] = mma_x2(ka[kk & 1][ti], mb[c][kk], kk == 0 ? zero4() : km[c][ti]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // ---- R = diag(beta) V - diag(beta e^G) (K M0), split by 32-row halves
+  hook(NK + 1);
+  bf16x8 kt0[NT], kt1[NT];
+  Frag rb[NC][2];
+  auto make_rb = [&](int h) __attribute__((always_inline)) {
+    f32x4 R[NC][2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const int ti = 2 * h + u;
+      const f32x4 bta = *reinterpret_cast<const f32x4*>(sc + 0 * kChunk + 16 * ti + 4 * lg);
+      const f32x4 bge = *reinterpret_cast<const f32x4*>(sc + 1 * kChunk + 16 * ti + 4 * lg);
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) R[c][u][r] = bta[r] * bf16_elt(vraw[c][ti], r) - bge[r] * km[c][ti][r];
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) rb[c][h] = chain_frag(R[c][0], R[c][1]);
+  };
+  make_rb(0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- Delta = hi(T) R, k step 0 | R rows 32..63; K^T for tokens 0..31 arrives
+  hook(NK + 2);
+#pragma unroll
+  for (int td = 0; td < NT; ++td) kt0[td] = ldkt(td, 0);
+  f32x4 D[NC][4];
+#pragma unroll
+  for (int ti = 0; ti < 4; ++ti)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) D[c][ti] = mma_x2(tfr[tri_frag(ti, 0)], rb[c][0], zero4());
+  make_rb(1);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- Delta, k step 1 for row tiles 2, 3 | the weighted Delta rows 0..31,
+  //      split; K^T for tokens 32..63 arrives
+  hook(NK + 3);
+#pragma unroll
+  for (int td = 0; td < NT; ++td) kt1[td] = ldkt(td, 1);
+#pragma unroll
+  for (int ti = 2; ti < 4; ++ti)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) D[c][ti] = mma_x2(tfr[tri_frag(ti, 1)], rb[c][1], D[c][ti]);
+  Frag db[NC][2];
+  auto make_db = [&](int h) __attribute__((always_inline)) {
+    f32x4 Dw[NC][2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      const f32x4 w = *reinterpret_cast<const f32x4*>(sc + 2 * kChunk + 16 * (2 * h + u) + 4 * lg);
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) Dw[c][u][r] = w[r] * D[c][2 * h + u][r];
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c) db[c][h] = chain_frag(Dw[c][0], Dw[c][1]);
+  };
+  make_db(0);
+  const float eg = sc[4 * kChunk];
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- M1 = e^{G_last} M0 + K^T Dw, tokens 0..31 | weighted Delta rows 32..63
+  hook(NK + 4);
+#pragma unroll
+  for (int td = 0; td < NT; ++td)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) M[c][td][r] *= eg;
+      M[c][td] = mma_x2(kt0[td], db[c][0], M[c][td]);
+    }
+  make_db(1);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- tokens 32..63 | split of M1 for the next chunk
+  hook(NK + 5);
+#pragma unroll
+  for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      M[c][2 * kk] = mma_x2(kt1[2 * kk], db[c][1], M[c][2 * kk]);
+      M[c][2 * kk + 1] = mma_x2(kt1[2 * kk + 1], db[c][1], M[c][2 * kk + 1]);
+      mb[c][kk] = chain_frag(M[c][2 * kk], M[c][2 * kk + 1]);
+    }
 }
 
 // Shared set-up of a scan workgroup for sequence n, value head h, state
@@ -529,15 +688,17 @@ constexpr int cols_threads(bool fwd, bool split) { return (fwd ? (split ? 4 : 5)
 template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup>
 using ColsLds = ScanLds<TIn, DK, COLS, FWD, true>;
 
-// Tail replay without outputs also comes 64 columns wide: four compute waves,
-// one per SIMD, and a DMA wave.  A wave's chunk takes as long as in the 32-wide
-// workgroup (each SIMD still runs one chain), so a CU advances twice the
-// columns per chunk: the choice for grids that do not fit on the chip at once
-// (a 64-wide workgroup moves 52 KiB of records and values per chunk for 64
-// columns; the whole-head kernel's eight waves each read 44 KiB of them from
-// LDS for 128 columns and are held back by it).
-constexpr int kColsWide = 64;
-constexpr int cols_wide_threads() { return (kColsWide / 16 + 1) * kWave; }
+// Tail replay of bf16 inputs whose grid does not fit on the chip at once (a
+// throughput batch) runs the wide column scan: COLS = 128 columns (a whole
+// head; 64 for d_v = 64) per workgroup, two 16-column tiles per compute wave
+// (chunk_step_tiles: the K, T and K^T operands are read from LDS once for both
+// tiles), no DMA wave (each compute wave issues a share of the next chunk's
+// DMA), and two workgroups per CU, so every SIMD holds two waves whose chains
+// interleave.  Measured on MI355X (16 sequences x 32 heads x 52 chunks):
+// 1.25x the columns per CU per unit time of the 64-column workgroup of four
+// one-tile waves and a DMA wave it replaces.
+constexpr int kWideTiles = 2;   // 16-column tiles per compute wave
+constexpr int cols_wide_threads(int cols) { return cols / (16 * kWideTiles) * kWave; }
 
 // Tail replay in two halves: the recurrence over a chunk is affine in the
 // state, M1 = A_c M0 + B_c with A_c = e^{G_last} I - K^T diag(e^{G_last - G}) T
@@ -562,9 +723,13 @@ struct SplitOut {
 __device__ __forceinline__ int split_point(int nch) { return (24 * nch + 21) / 43; }
 
 // One column-split workgroup (block `block` of `nblocks`), LDS in `lds`, COLS
-// columns per workgroup.  Waves 0 .. COLS/16 - 1 compute, the next issues the
-// DMA; any further waves of the workgroup only take part in the barriers.
-template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup, int PART = kWhole>
+// columns per workgroup, NC tiles of 16 columns per compute wave.  Waves 0 ..
+// COLS / (16 NC) - 1 compute.  With DMA_WAVE the next issues the DMA and any
+// further waves only take part in the barriers; without, the compute waves
+// issue the next chunk's DMA themselves, a share at each phase of the chunk
+// (multi-tile steps only).
+template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup, int PART = kWhole, int NC = 1,
+          bool DMA_WAVE = true>
 __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int nblocks,
                                                const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                                int32_t dv, const TIn* __restrict__ v,
@@ -578,13 +743,15 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
   constexpr bool SPLIT = PART != kWhole;
   static_assert(!(SPLIT && FWD), "the split form is tail replay only");
   constexpr int NT = DK / 16;
-  constexpr int CW = COLS / 16;   // compute waves
+  constexpr int CW = COLS / (16 * NC);   // compute waves
+  static_assert(CW * 16 * NC == COLS, "whole column tiles per wave");
+  static_assert(DMA_WAVE || NC > 1, "the compute waves issue the DMA in multi-tile steps");
   constexpr int kVJob0 = L::kKJobs + L::kTJobs + L::kPJobs;   // first V job
   const int tid = threadIdx.x;
   // wave index made provably uniform: DMA destinations (M0) stay scalar
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
-  const bool data_wave = wave >= CW;
-  const bool dma_wave = wave == CW;
+  const bool data_wave = DMA_WAVE && wave >= CW;
+  const bool dma_wave = DMA_WAVE && wave == CW;
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
   const int ngroups = PART == kSecondHalf ? dv / COLS + DK / COLS : dv / COLS;
   // logical unit: the column groups of a value head, then the value heads of a
@@ -609,7 +776,7 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
     }
   }
   const int col0 = COLS * g;
-  const int col = col0 + 16 * wave + lr;
+  const int colw = col0 + 16 * NC * wave;   // the wave's first column; tile c: colw + 16 c + lr
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
   auto dma_chunk = [&](int ci, int b) __attribute__((always_inline)) {
     const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, ident ? 0 : col0, v, kin, qin, Kw, Tw, Sw, Pw);
@@ -620,80 +787,124 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
       dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
     }
   };
-
-  f32x4 M[NT];
-  Frag mb[DK / 32];
-  f32x4 pout[4];
-  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * ld + col;
-  if constexpr (SPLIT) {
-    if (ident) {
-      // M0 = identity columns; V tiles of both buffers zero
-      if (!data_wave) {
+  // without a DMA wave: this compute wave's jobs wave + CW jj, jj in [j0, j1)
+  constexpr int PER_WAVE = (L::kJobs + CW - 1) / CW;
+  auto dma_share = [&](int ci, int b, int j0, int j1) __attribute__((always_inline)) {
+    const ChunkSrc c = chunk_src<L>(u, ci, hk, hv, dv, ident ? 0 : col0, v, kin, qin, Kw, Tw, Sw, Pw);
 #pragma unroll
-        for (int td = 0; td < NT; ++td)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) M[td][r] = (strow(td, lg, r) == col) ? 1.f : 0.f;
-#pragma unroll
-        for (int kk = 0; kk < DK / 32; ++kk) mb[kk] = chain_frag(M[2 * kk], M[2 * kk + 1]);
-      }
-      for (int b = 0; b < L::kBuffers; ++b)
-        for (int x = 16 * tid; x < L::kVBytes; x += 16 * static_cast<int>(blockDim.x))
-          *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(lds_l + b * L::kBytes + L::kOffV + x) =
-              u32x4{0u, 0u, 0u, 0u};
-    } else if (!data_wave) {
-      load_state<DK>(nullptr, sbase, ld, lg, M, mb);
+    for (int jj = j0; jj < j1; ++jj) {
+      const int j = wave + CW * jj;
+      if (j >= L::kJobs || (SPLIT && ident && j >= kVJob0 && j < kVJob0 + L::kVJobs)) continue;
+      dma_job<L, TIn>(c, vrow, lds_l + b * L::kBytes, j, lane);
     }
-  } else {
-    if (!data_wave) load_state<DK>(state_in, sbase, dv, lg, M, mb);
+  };
+
+  const int64_t sbase = (static_cast<int64_t>(u.n) * hv + u.h) * DK * ld + colw + lr;   // tile c: + 16 c
+  if (SPLIT && ident) {
+    // the transition's V tiles (both buffers) are zero
+    for (int b = 0; b < L::kBuffers; ++b)
+      for (int x = 16 * tid; x < L::kVBytes; x += 16 * static_cast<int>(blockDim.x))
+        *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(lds_l + b * L::kBytes + L::kOffV + x) =
+            u32x4{0u, 0u, 0u, 0u};
+  }
+  const int nch = ce - cb;
+  // The data waves and the compute waves run loops of their own with the same
+  // barriers (two per chunk with one buffer, else one), so the state lives in
+  // the compute waves' loop alone.
+  if (data_wave) {
+    if (dma_wave && nch > 0) {
+      dma_chunk(cb, 0);
+      wait_dma();
+    }
+    __syncthreads();
+    for (int j = 0; j < nch; ++j) {
+      const int b = L::kBuffers == 2 ? (j & 1) : 0;
+      if (dma_wave && L::kBuffers == 2 && j + 1 < nch) {
+        dma_chunk(cb + j + 1, b ^ 1);   // lands while the compute waves work on buffer b
+        wait_dma();
+      }
+      if (L::kBuffers == 1) {
+        __syncthreads();   // the compute waves are done with the only buffer
+        if (dma_wave && j + 1 < nch) {
+          dma_chunk(cb + j + 1, 0);
+          wait_dma();
+        }
+      }
+      __syncthreads();     // next chunk's operands are in LDS; this buffer is free
+    }
+    return;
   }
 
-  const int nch = ce - cb;
-  if (dma_wave && nch > 0) {
-    dma_chunk(cb, 0);
+  f32x4 M[NC][NT];
+  Frag mb[NC][DK / 32];
+  f32x4 pout[4];
+  if (SPLIT && ident) {
+    // M0 = identity columns
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+#pragma unroll
+      for (int td = 0; td < NT; ++td)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) M[c][td][r] = (strow(td, lg, r) == colw + 16 * c + lr) ? 1.f : 0.f;
+#pragma unroll
+      for (int kk = 0; kk < DK / 32; ++kk) mb[c][kk] = chain_frag(M[c][2 * kk], M[c][2 * kk + 1]);
+    }
+  } else {
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+      load_state<DK>(SPLIT ? nullptr : state_in, sbase + 16 * c, ld, lg, M[c], mb[c]);
+  }
+  if (!DMA_WAVE && nch > 0) {
+    dma_share(cb, 0, 0, PER_WAVE);
     wait_dma();
   }
   __syncthreads();
   for (int j = 0; j < nch; ++j) {
     const int ci = cb + j;
     const int b = L::kBuffers == 2 ? (j & 1) : 0;
-    if (data_wave) {
-      if (dma_wave && L::kBuffers == 2 && j + 1 < nch) {
-        dma_chunk(ci + 1, b ^ 1);   // lands while the compute waves work on buffer b
-        wait_dma();
-      }
+    if constexpr (FWD) {
+      if (j > 0) store_chunk_out(o, u, ci - 1, hv, dv, colw, lane, pout);
+    }
+    const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
+    const unsigned char* buf = (const unsigned char*)(lds_l + b * L::kBytes);
+    if constexpr (NC > 1) {
+      // without a DMA wave: the next chunk's share, spread over the phases
+      const bool prefetch = !DMA_WAVE && L::kBuffers == 2 && j + 1 < nch;
+      constexpr int NPH = tiles_phases(DK);
+      chunk_step_tiles<L, DK, NC>(buf, 16 * NC * wave, lane, M, mb, [&](int p) __attribute__((always_inline)) {
+        const int j0 = p * PER_WAVE / NPH, j1 = (p + 1) * PER_WAVE / NPH;
+        if (prefetch && j1 > j0) dma_share(ci + 1, b ^ 1, j0, j1);
+      });
+      if (!DMA_WAVE) wait_dma();   // this wave's share of the next chunk has landed
     } else {
-      if constexpr (FWD) {
-        if (j > 0) store_chunk_out(o, u, ci - 1, hv, dv, col - lr, lane, pout);
-      }
-      const u32x4* pg = FWD ? Pw + (static_cast<int64_t>(u.slot0 + ci) * hv + u.h) * (2 * kTFrags * kWave) : nullptr;
-      chunk_step<L, DK, FWD, false>((const unsigned char*)(lds_l + b * L::kBytes), 16 * wave, pg, lane, M, mb,
-                                    pout, [](int) {});
+      chunk_step<L, DK, FWD, false>(buf, 16 * wave, pg, lane, M[0], mb[0], pout, [](int) {});
     }
     if (L::kBuffers == 1) {
-      __syncthreads();   // the compute waves are done with the only buffer
-      if (dma_wave && j + 1 < nch) {
-        dma_chunk(ci + 1, 0);
+      __syncthreads();   // done with the only buffer
+      if (!DMA_WAVE && j + 1 < nch) {
+        dma_share(ci + 1, 0, 0, PER_WAVE);
         wait_dma();
       }
     }
-    __syncthreads();     // next chunk's operands are in LDS; this buffer is free
+    __syncthreads();     // next chunk's operands are in LDS (every wave's share)
   }
-  if (!data_wave) {
-    if constexpr (FWD) {
-      if (nch > 0) store_chunk_out(o, u, ce - 1, hv, dv, col - lr, lane, pout);
-    }
+  if constexpr (FWD) {
+    if (nch > 0) store_chunk_out(o, u, ce - 1, hv, dv, colw, lane, pout);
+  }
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
     if (SPLIT && ident) {
       // the transition goes out transposed, A^T [d_k x d_k]: a lane's four
-      // rows of column `col` are one 16-byte piece of row `col` of A^T
-      float* at = dst + ((static_cast<int64_t>(u.n) * hv + u.h) * DK + col) * DK;
+      // rows of its column are one 16-byte piece of that row of A^T
+      float* at = dst + ((static_cast<int64_t>(u.n) * hv + u.h) * DK + colw + 16 * c + lr) * DK;
 #pragma unroll
-      for (int td = 0; td < NT; ++td) *reinterpret_cast<f32x4*>(at + strow(td, lg, 0)) = M[td];
+      for (int td = 0; td < NT; ++td) *reinterpret_cast<f32x4*>(at + strow(td, lg, 0)) = M[c][td];
     } else if (dst) {
 #pragma unroll
       for (int td = 0; td < NT; ++td)
 #pragma unroll
         for (int r = 0; r < 4; ++r)
-          dst[sbase + static_cast<int64_t>(strow(td, lg, r)) * ld] = M[td][r];
+          dst[sbase + 16 * c + static_cast<int64_t>(strow(td, lg, r)) * ld] = M[c][td][r];
     }
   }
 }
@@ -935,46 +1146,47 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   }
 }
 
-// The 64-wide column scan, tail replay only (grid N x Hv x d_v / 64).
-template <typename TIn, int DK>
-__global__ __launch_bounds__(cols_wide_threads())
+// The wide column scan, tail replay only (grid N x Hv x d_v / COLS).
+template <typename TIn, int DK, int COLS>
+__global__ __launch_bounds__(cols_wide_threads(COLS)) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
                       const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
-                 const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                      const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                       const float* __restrict__ Sw, float* __restrict__ state_out) {
-  using L = ColsLds<TIn, DK, false, kColsWide>;
+  using L = ColsLds<TIn, DK, false, COLS>;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
-  scan_cols_body<TIn, DK, false, kColsWide>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin,
-                                            Kw, Tw,
-                                            Sw, nullptr, nullptr, nullptr, state_out, SplitOut{}, &order);
+  scan_cols_body<TIn, DK, false, COLS, kWhole, kWideTiles, false>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk,
+                                                                  hv, dv, v, kin, qin, Kw, Tw, Sw, nullptr,
+                                                                  nullptr, nullptr, state_out, SplitOut{}, &order);
 }
 
 // Tail replay in two halves, one launch: blocks [0, n_first) run the first
-// half 32 columns wide (grid N x Hv x d_v / 32; waves 3 and 4 only take part
-// in the barriers), the rest the second half and its transition 64 columns
-// wide (N x Hv x (d_v + d_k) / 64).  state_out holds the first half's state
-// until k_state_combine runs.
+// half kSplitCols1 = 32 columns wide (grid N x Hv x d_v / 32; waves 3 and 4
+// only take part in the barriers), the rest the second half and its
+// transition kSplitCols2 = 64 columns wide (N x Hv x (d_v + d_k) / 64), one
+// 16-column tile per compute wave.  state_out holds the first half's state
+// until the combine runs.
+constexpr int cols_split_threads() { return (kSplitCols2 / 16 + 1) * kWave; }
 template <typename TIn, int DK>
-__global__ __launch_bounds__(cols_wide_threads())
+__global__ __launch_bounds__(cols_split_threads())
 void k_scan_cols_split(int32_t n_first, const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
                        const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                        const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                        const float* __restrict__ Sw, float* __restrict__ state_out, float* __restrict__ m2,
                        float* __restrict__ a2) {
-  using L1 = ColsLds<TIn, DK, false, kColsPerGroup>;
-  using L2 = ColsLds<TIn, DK, false, kColsWide>;
+  using L1 = ColsLds<TIn, DK, false, kSplitCols1>;
+  using L2 = ColsLds<TIn, DK, false, kSplitCols2>;
   constexpr int kB1 = L1::kBuffers * L1::kBytes, kB2 = L2::kBuffers * L2::kBytes;
   __shared__ __attribute__((aligned(1024))) unsigned char lds[kB1 > kB2 ? kB1 : kB2];
   const int b = blockIdx.x;
   if (b < n_first)
-    scan_cols_body<TIn, DK, false, kColsPerGroup, kFirstHalf>((lds_byte*)lds, b, n_first, cu, hk, hv, dv, v,
-                                                              kin, qin, Kw, Tw, Sw, nullptr, nullptr, nullptr,
-                                                              state_out);
+    scan_cols_body<TIn, DK, false, kSplitCols1, kFirstHalf>((lds_byte*)lds, b, n_first, cu, hk, hv, dv, v, kin, qin,
+                                                            Kw, Tw, Sw, nullptr, nullptr, nullptr, state_out);
   else
-    scan_cols_body<TIn, DK, false, kColsWide, kSecondHalf>((lds_byte*)lds, b - n_first,
-                                                           static_cast<int>(gridDim.x) - n_first, cu, hk, hv,
-                                                           dv, v, kin, qin, Kw, Tw, Sw, nullptr, nullptr, nullptr,
-                                                           nullptr, SplitOut{m2, a2});
+    scan_cols_body<TIn, DK, false, kSplitCols2, kSecondHalf>((lds_byte*)lds, b - n_first,
+                                                             static_cast<int>(gridDim.x) - n_first, cu, hk, hv, dv, v,
+                                                             kin, qin, Kw, Tw, Sw, nullptr, nullptr, nullptr, nullptr,
+                                                             SplitOut{m2, a2});
 }
 
 // state = A state + B per (sequence, value head): A^T [d_k x d_k], state and

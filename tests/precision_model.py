@@ -14,11 +14,14 @@ multiplied in the passes a variant names:
     ktd  K^T Dw      "2": K^T (hi + lo)(Dw)         "1": K^T hi(Dw)
     qm   Q M0        "2": Q (hi + lo)(M0)           "1": Q hi(M0)
     pd   P Delta     "3", "2a", "2b", "1" as for T R (P in the place of T)
-Results are rounded to fp32 where the kernels hold fp32 (R, Delta, M1) and
-outputs to the storage dtype (``out_bf16``).  The model covers bf16 inputs (K
-and Q exact operands).  The kernels' choice for bf16 inputs is ``KERNEL``:
-km=2, tr=2a, ktd=2, qm=2, pd=3 (``ALL_PASSES`` is the three-pass form they
-used before).
+With ``fold`` (tail replay, no outputs) the row weights would go into T
+before it is split: T~ = diag(e^{G_last - G}) T diag(beta), R~ = V - diag(e^G)
+K M0 and Dw = T~ R~ directly; the kernels do not do this, since hi(T~) loses
+the exact unit diagonal that hi(T) keeps.  Results are rounded to fp32 where
+the kernels hold fp32 (R, Delta, M1) and outputs to the storage dtype
+(``out_bf16``).  The model covers bf16 inputs (K and Q exact operands).  The
+kernels' choice for bf16 inputs is ``KERNEL``: km=2, tr=2a, ktd=2, qm=2, pd=3
+(``ALL_PASSES`` is the three-pass form they used before).
 """
 from __future__ import annotations
 
@@ -38,6 +41,7 @@ class Passes:
     ktd: str = "2"
     qm: str = "2"
     pd: str = "3"
+    fold: bool = False
 
 
 ALL_PASSES = Passes()
@@ -106,6 +110,13 @@ def run(k, v, g, beta, q=None, m0=None, scale=1.0, passes: Passes = KERNEL, out_
         Tm = _f32(np.linalg.inv(np.eye(C) + A))
         ms = split(M)
         KM = _mm_exact_split(K, ms, passes.km)
+        w = np.exp(G[-1] - G)
+        if passes.fold and q is None:
+            Tw = _f32(w[:, None] * Tm * bb[None, :])
+            R = _f32(V - np.exp(G)[:, None] * KM)
+            Dw = _f32(_mm_split_split(split(Tw), split(R), passes.tr))
+            M = _f32(np.exp(G[-1]) * M + _mm_exact_split(K.T, split(Dw), passes.ktd))
+            continue
         R = _f32(bb[:, None] * V - (bb * np.exp(G))[:, None] * KM)
         D = _f32(_mm_split_split(split(Tm), split(R), passes.tr))
         if q is not None:
@@ -115,7 +126,6 @@ def run(k, v, g, beta, q=None, m0=None, scale=1.0, passes: Passes = KERNEL, out_
             QM = _mm_exact_split(Q, ms, passes.qm)
             O = _f32(scale * np.exp(G)[:, None] * QM + _mm_split_split(split(P), split(D), passes.pd))
             outs[c0:c0 + n] = _bf16(O[:n]) if out_bf16 else O[:n]
-        w = np.exp(G[-1] - G)
         Dw = w[:, None] * D
         M = _f32(np.exp(G[-1]) * M + _mm_exact_split(K.T, split(Dw), passes.ktd))
     return outs, M

@@ -170,10 +170,11 @@ def test_adversarial_repeated_keys():
 
 def test_whole_head_and_column_kernels_agree():
     # 72 sequences x 4 heads exceed the chip with the column-split scan (one
-    # workgroup per 32 columns), so the batch's tail replay runs on the 64-wide
-    # column scan and its forward on the whole-head kernel; single sequences
-    # run on the 32-wide column scan.  Same arithmetic per wave: the replayed
-    # states agree bit for bit.
+    # workgroup per 32 columns), so the batch's tail replay runs on the wide
+    # column scan (two tiles per wave) and its forward on the whole-head
+    # kernel; single sequences run on the 32-wide column scan (one tile per
+    # wave).  Same products in the same order: the replayed states agree bit
+    # for bit.
     lens = [1 + (37 * i) % 200 for i in range(72)]
     seqs = [_seq(i, n) for i, n in enumerate(lens)]
     x = device_inputs(synth.pack(seqs))
@@ -186,7 +187,7 @@ def test_whole_head_and_column_kernels_agree():
         sti = gdn.tail_replay(xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"], xi["cu_host"])
         oi, _ = gdn.chunk_forward(xi["q"], xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"],
                                   xi["cu_host"], state_in=sti)
-        assert torch.equal(st[i:i + 1], sti), f"sequence {i}: 64-wide and 32-wide replays differ"
+        assert torch.equal(st[i:i + 1], sti), f"sequence {i}: wide and 32-wide replays differ"
         a, b = int(cu[i]), int(cu[i + 1])
         rel = (o[a:b].float() - oi.float()).norm() / oi.float().norm()
         assert rel.item() <= 1e-3   # bf16 outputs: one rounding step apart at most
@@ -266,7 +267,7 @@ def test_split_replay_agrees_with_one_chain(r, slow):
 
 
 def test_varlen_graph_with_longest_first_order():
-    """An unsorted varlen batch whose scan grids exceed the chip (64-wide tail
+    """An unsorted varlen batch whose scan grids exceed the chip (wide tail
     scan, whole-head forward): both run in longest-first order, which travels
     in the kernels' arguments.  Tail replay and forward captured in one HIP
     graph replay bitwise like the eager calls, three times, with other eager

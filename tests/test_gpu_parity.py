@@ -62,7 +62,7 @@ def test_ragged_varlen(dtype, dk, dv, grp):
 # 72 short sequences: with 4 value heads the column-split grid is 72 x 4 x d_v/32
 # >= 576 workgroups, more than the 256 CUs, so the forward runs on the
 # whole-head scan kernel, and so does the fp32 tail replay; the bf16 tail
-# replay runs on the 64-wide column scan (d_v = 64: one group per head)
+# replay runs on the wide column scan (two 16-column tiles per wave)
 WIDE_LENS = [1 + (37 * i) % 200 for i in range(72)]
 
 
@@ -197,7 +197,7 @@ def test_workload2_layer_stack_sampled():
     """The 36-layer stack (prefix 32768, tail 3277, suffix 1024) in both launch
     forms the benchmark times: per layer, the tail replay (split in two
     halves at this length) then the suffix forward from the rebuilt state; and
-    the 36 layers as one batched tail replay (the 64-wide column scan, 36 x 52
+    the 36 layers as one batched tail replay (the wide column scan, 36 x 52
     chunks in one launch) then one batched suffix forward (the whole-head
     scan).  Sampled (layer, value head) units against the oracle: the rebuilt
     state, the suffix outputs and the final state."""
