@@ -1148,7 +1148,7 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
 
 // The wide column scan, tail replay only (grid N x Hv x d_v / COLS).
 template <typename TIn, int DK, int COLS>
-__global__ __launch_bounds__(cols_wide_threads(COLS)) __attribute__((amdgpu_waves_per_eu(2, 2)))
+__global__ __launch_bounds__(cols_wide_threads(COLS)) __attribute__((amdgpu_waves_per_eu(COLS / 64, 2)))
 void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
                       const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                       const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
