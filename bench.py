@@ -17,7 +17,9 @@ scan), launched eagerly on one stream.  ``value`` = tokens through the path per
 second, 36 x (3277 + 1024) per step.  Beside it: the same step as two calls
 per layer (``gdn_tail_replay`` + ``gdn_chunk_forward``, bit for bit the same
 results) and replayed from a HIP graph, the 36 layers as one batched call
-(layers as sequences), the
+(layers as sequences), the 36 layers as a hybrid model's 12 groups of 3 GDN
+layers (groups replay independently, paper Section 3: one fused call per
+depth with that depth's 12 layers as its sequences, the 3 depths in order), the
 rebuild latency of the 36 replays (warm, cold, queued), per-stage kernel
 durations from HIP events that the library records on the stream its kernels
 run on, ``roofline`` for the dominant kernel, the one-layer workload
@@ -50,6 +52,7 @@ CHUNK = 64
 CALIB_BYTES = 1 << 30          # plain copy used to calibrate the PMC byte counters (> the 256 MB MALL)
 FLUSH_BYTES = 512 << 20        # > 256 MB Infinity Cache: evicts it between cold reps
 QUEUE_SPIN_CYCLES = 2_000_000  # spin kernel (~0.8 ms) that outlasts the host's enqueue of one call
+GROUP_DEPTH = 3                # GDN layers per hybrid-model group in the grouped form (3 GDN : 1 FA)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic_workload2.json")
 KERNEL_SOURCES = ("include/gdn_tail_replay.h", "paper_2608_30310_amd/csrc/gdn_plan.h",
                   "paper_2608_30310_amd/csrc/gdn_plan.cpp", "paper_2608_30310_amd/csrc/gdn_device.h",
@@ -360,8 +363,45 @@ def main():
         gdn.chunk_forward(xs["q"], xs["k"], xs["v"], xs["g"], xs["beta"], xs["cu"], xs["cu_host"],
                           state_in=midb, o=ob, state_out=finb, workspace=ws_bf)
 
+    # the layers as a hybrid model's groups (paper Section 3: one FA layer and
+    # the GDN layers after it; each group replays on its own, from the cached
+    # FA output hidden): GROUP_DEPTH GDN layers per group, so the layers of one
+    # depth, one per group, run as the sequences of one fused call, and the
+    # depths run in sequence (a layer's inputs come from the one before it)
+    depth_calls = []
+    for dd in range(min(GROUP_DEPTH, L)):
+        lays = list(range(dd, L, GROUP_DEPTH))
+        n = len(lays)
+        tk = {nm: torch.cat([xt[nm][l * r:(l + 1) * r] for l in lays]) for nm in ("k", "v", "g", "beta")}
+        sk = {nm: torch.cat([xs[nm][l * s:(l + 1) * s] for l in lays]) for nm in ("q", "k", "v", "g", "beta")}
+        cut_l, cus_l = [r * i for i in range(n + 1)], [s * i for i in range(n + 1)]
+        depth_calls.append(dict(
+            lays=lays, t=tk, s=sk,
+            cut=torch.tensor(cut_l, dtype=torch.int32, device=dev), cut_h=torch.tensor(cut_l, dtype=torch.int32),
+            cus=torch.tensor(cus_l, dtype=torch.int32, device=dev), cus_h=torch.tensor(cus_l, dtype=torch.int32),
+            mid=torch.empty((n, hv, dk, dv), dtype=torch.float32, device=dev),
+            fin=torch.empty((n, hv, dk, dv), dtype=torch.float32, device=dev),
+            o=torch.empty((n * s, hv, dv), dtype=torch.bfloat16, device=dev),
+            ws=torch.empty(gdn.replay_forward_workspace_size(n, hk, hv, dk, dv, cut_l, cus_l) + 256,
+                           dtype=torch.uint8, device=dev),
+            ws_t=torch.empty(gdn.workspace_size(n, hk, hv, dk, dv, cut_l) + 256, dtype=torch.uint8, device=dev)))
+
+    def grouped_step():
+        for c in depth_calls:
+            a, b = c["t"], c["s"]
+            gdn.replay_forward(a["k"], a["v"], a["g"], a["beta"], c["cut"], b["q"], b["k"], b["v"], b["g"],
+                               b["beta"], c["cus"], cu_tail_host=c["cut_h"], cu_suf_host=c["cus_h"],
+                               state_mid=c["mid"], o=c["o"], state_out=c["fin"], workspace=c["ws"])
+
+    def grouped_replay():
+        for c in depth_calls:
+            a = c["t"]
+            gdn.tail_replay(a["k"], a["v"], a["g"], a["beta"], c["cut"], c["cut_h"], state_out=c["mid"],
+                            workspace=c["ws_t"])
+
     for _ in range(args.warmup):
         step()
+        grouped_step()
         if not args.no_batched:
             batched_step()
     torch.cuda.synchronize()
@@ -413,13 +453,23 @@ def main():
     if not args.no_batched:
         batched_step()
         torch.cuda.synchronize()
-        bdiff = float(((finb - want[1]).norm() / want[1].norm()).item())
+        bdiff = [float(((x - w).norm() / w.norm()).item()) for x, w in ((midb, want[0]), (finb, want[1]))]
+    grouped_step()
+    torch.cuda.synchronize()
+    mid_g, fin_g = torch.empty_like(mid), torch.empty_like(fin)
+    for c in depth_calls:
+        mid_g[c["lays"]] = c["mid"]
+        fin_g[c["lays"]] = c["fin"]
+    gdiff = [float(((x - w).norm() / w.norm()).item()) for x, w in ((mid_g, want[0]), (fin_g, want[1]))]
+    del mid_g, fin_g
 
     ms_per_step = timed(step)
     ms_graph = timed(graph.replay) if graph is not None else None
     ms_two_calls = timed(two_calls_step)
     ms_batched = None if args.no_batched else timed(batched_step)
     ms_batched_rebuild = None if args.no_batched else timed(batched_replay)
+    ms_grouped = timed(grouped_step)
+    ms_grouped_rebuild = timed(grouped_replay)
 
     # ---- per-stage kernel durations: events recorded by the library on its stream
     n_ev = min(K, 20)
@@ -543,12 +593,20 @@ def main():
         "ms_per_step_two_calls": ms_two_calls,
         "two_calls_bitwise_equal": two_calls_equal,
         "ms_per_step_batched": ms_batched,
-        "batched_vs_sequential_rel_state_diff": bdiff,
+        # relative Frobenius differences of the rebuilt (tail) states and the
+        # final states: the forms differ in rounding order only (the final
+        # states agree once the suffix's decay has erased the difference)
+        "batched_vs_sequential_rel_state_diff": None if bdiff is None else {"tail": bdiff[0], "final": bdiff[1]},
+        "ms_per_step_grouped": ms_grouped,
+        "grouped": f"{len(depth_calls[0]['lays'])} groups of {GROUP_DEPTH} layers: one fused call per depth, "
+                   "the depth's layers as its sequences",
+        "grouped_vs_sequential_rel_state_diff": {"tail": gdiff[0], "final": gdiff[1]},
         "rebuild_latency_us": warm["p50"],
         "rebuild_latency_warm_us": warm,
         "rebuild_latency_cold_us": cold,
         "rebuild_latency_queued_us": queued_rebuild,
         "rebuild_latency_batched_us": None if ms_batched_rebuild is None else ms_batched_rebuild * 1e3,
+        "rebuild_latency_grouped_us": ms_grouped_rebuild * 1e3,
         "replay_tokens_per_s": L * r / (warm["p50"] * 1e-6),
         "replay_tokens_per_s_batched": None if ms_batched_rebuild is None else L * r / (ms_batched_rebuild * 1e-3),
         "stages": stages,
