@@ -154,10 +154,22 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
       return check_launch("state combine launch");
     }
   }
+  // with outputs and bf16 inputs, 16 columns per workgroup where even that grid fits
+  constexpr bool kNarrow = FWD && sizeof(TIn) == 2;
+  if constexpr (kNarrow) {
+    if (2 * col_groups <= static_cast<uint32_t>(cus)) {
+      hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD, 1>), dim3(2 * col_groups), dim3(cols_threads(FWD, false, 1)), 0,
+                         stream, cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
+                         static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in,
+                         static_cast<TIn*>(o), state_out);
+      return check_launch("scan launch");
+    }
+  }
   if (fits) {
-    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0, stream, cu,
-                       s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
-                       static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o), state_out);
+    hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0,
+                       stream, cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
+                       static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in,
+                       static_cast<TIn*>(o), state_out);
   } else if constexpr (kWide) {
     // a whole head per workgroup (128 columns, four compute waves) where d_v allows
     constexpr int kCols = DV >= 128 ? 128 : 64;

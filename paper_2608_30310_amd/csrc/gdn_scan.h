@@ -683,7 +683,9 @@ constexpr int kColsPerGroup = 32;
 // recurrence wave needs ~250 VGPRs, more than two waves sharing a SIMD may
 // hold, so the two output waves issue the DMA instead (4 waves).
 constexpr bool cols_dma_wave(bool fwd, bool split) { return fwd && !split; }
-constexpr int cols_threads(bool fwd, bool split) { return (fwd ? (split ? 4 : 5) : 3) * kWave; }
+constexpr int cols_threads(bool fwd, bool split, int tiles = 2) {
+  return (fwd ? (split ? 4 : 1 + 2 * tiles) : 3) * kWave;
+}
 
 template <typename TIn, int DK, bool FWD, int COLS = kColsPerGroup>
 using ColsLds = ScanLds<TIn, DK, COLS, FWD, true>;
@@ -912,15 +914,15 @@ __device__ __forceinline__ void scan_cols_body(lds_byte* lds_l, int block, int n
 // LDS of the workgroup with outputs: chunk buffers (P read from global
 // memory) and, per 16-column tile, the exchange from the recurrence wave to
 // the output wave: Delta (4 KiB) and the split state (d_k / 32 x 2 KiB).
-template <typename TIn, int DK>
+template <typename TIn, int DK, int TILES = 2>
 struct ColsOutLayout {
-  using L = ScanLds<TIn, DK, kColsPerGroup, true, false>;
+  using L = ScanLds<TIn, DK, 16 * TILES, true, false>;
   static constexpr int kDBytes = 4 * kWave * 16;
   static constexpr int kMBytes = DK / 32 * 2 * kWave * 16;
   static constexpr int kTileBytes = kDBytes + kMBytes;
-  static constexpr int kBuffers = 2 * L::kBytes + 2 * kTileBytes <= kLdsBytes ? 2 : 1;
+  static constexpr int kBuffers = 2 * L::kBytes + TILES * kTileBytes <= kLdsBytes ? 2 : 1;
   static constexpr int kOffX = kBuffers * L::kBytes;
-  static constexpr int kBytes = kOffX + 2 * kTileBytes;
+  static constexpr int kBytes = kOffX + TILES * kTileBytes;
   static_assert(kBytes <= kLdsBytes, "column scan with outputs does not fit in LDS");
 };
 
@@ -938,8 +940,11 @@ struct ColsOutLayout {
 // wave has one to itself.  Without (fp32 inputs): waves c carry the
 // recurrence, waves 2 + c write the outputs and each issues half of the DMA.
 // The products are those of chunk_step with outputs, in the same order, so the
-// results are the same bit for bit.
-template <typename TIn, int DK>
+// results are the same bit for bit.  TILES = 1 (bf16 inputs): a 16-column
+// workgroup of a DMA wave, one recurrence wave and one output wave, for grids
+// that fit on the chip at one workgroup per CU even so (each recurrence wave
+// then has a CU's LDS bandwidth to itself).
+template <typename TIn, int DK, int TILES = 2>
 __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, int nblocks,
                                                    const int32_t* __restrict__ cu, int32_t hk, int32_t hv,
                                                    int32_t dv, const TIn* __restrict__ v,
@@ -948,13 +953,14 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
                                                    const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                    const float* __restrict__ state_in, TIn* __restrict__ o,
                                                    float* __restrict__ state_out) {
-  using CL = ColsOutLayout<TIn, DK>;
+  using CL = ColsOutLayout<TIn, DK, TILES>;
   using L = typename CL::L;
   constexpr bool SPLIT = L::kSplit;
   constexpr int NT = DK / 16, NK = DK / 32;
   constexpr int NKA = ka_frags(DK);
   constexpr int NKF = L::kKFrags;
   constexpr bool DMA_WAVE = cols_dma_wave(true, SPLIT);
+  static_assert(TILES == 2 || (TILES == 1 && DMA_WAVE), "one tile per workgroup needs the DMA wave");
   constexpr int kEarlyJobs = 2 * L::kJobs / 3;   // DMA jobs issued before the mid-chunk barrier
   static_assert(DMA_WAVE || (L::kKJobs % 2 == 0 && L::kTJobs % 2 == 0 && L::kPJobs == 0 &&
                              L::kVJobs % 2 == 0), "DMA halves need records of whole multiples of 2 KiB");
@@ -964,15 +970,16 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int first_chain = DMA_WAVE ? 1 : 0;
   const bool dma_wave = DMA_WAVE && wave == 0;
-  const bool chain_wave = wave == first_chain || wave == first_chain + 1;
-  const bool out_wave = wave >= first_chain + 2;
-  const int tile = (wave - first_chain) & 1, h = tile;
+  const bool chain_wave = wave >= first_chain && wave < first_chain + TILES;
+  const bool out_wave = wave >= first_chain + TILES;
+  const int tile = (wave - first_chain) % TILES, h = tile;
   const int lane = tid % kWave, lg = lane / 16, lr = lane % 16;
-  const int ngroups = dv / kColsPerGroup;
+  constexpr int COLS = 16 * TILES;
+  const int ngroups = dv / COLS;
   // logical unit: the column groups of a value head, then the value heads of a
   // key head, are adjacent and one cluster (same XCD, shared records in its L2)
   const int unit = xcd_cluster_remap(block, nblocks, ngroups * (hv / hk));
-  const int col0 = kColsPerGroup * (unit % ngroups);
+  const int col0 = COLS * (unit % ngroups);
   const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
   const int colw = col0 + 16 * tile;
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
@@ -1127,17 +1134,17 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   }
 }
 
-template <typename TIn, int DK, bool FWD>
-__global__ __launch_bounds__(cols_threads(FWD, sizeof(TIn) == 4)) __attribute__((amdgpu_waves_per_eu(1, 1)))
+template <typename TIn, int DK, bool FWD, int TILES = 2>
+__global__ __launch_bounds__(cols_threads(FWD, sizeof(TIn) == 4, TILES)) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t dv,
                  const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                  const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                  const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                  const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
   if constexpr (FWD) {
-    __shared__ __attribute__((aligned(1024))) unsigned char lds[ColsOutLayout<TIn, DK>::kBytes];
-    scan_cols_out_body<TIn, DK>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin, Kw, Tw, Sw, Pw,
-                                state_in, o, state_out);
+    __shared__ __attribute__((aligned(1024))) unsigned char lds[ColsOutLayout<TIn, DK, TILES>::kBytes];
+    scan_cols_out_body<TIn, DK, TILES>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin, Kw, Tw,
+                                       Sw, Pw, state_in, o, state_out);
   } else {
     using L = ColsLds<TIn, DK, false>;
     __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
