@@ -353,13 +353,24 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD>& sm, int slot,
     const int ti = f < 2 ? f : 2 + (f - 2) / 2, kk = f < 2 ? 0 : (f - 2) % 2;
     const int fg = fl / 16, fr = fl % 16;
     const int row = 16 * ti + fr;
-    float tv[8], pv[8];
+    // the lane's elements j < 4 are columns 32 kk + 4 fg .. + 3 (column block
+    // 2 kk) and j >= 4 the same 16 columns further (block 2 kk + 1): two
+    // 16-byte reads, conflict-free over each 16 lanes (rows 68 floats apart);
+    // blocks above the diagonal are zero
+    const int c0 = 32 * kk + 4 * fg;
+    const bool lo_blk = 2 * kk <= ti, hi_blk = 2 * kk + 1 <= ti;
+    const f32x4 t0 = lo_blk ? *reinterpret_cast<const f32x4*>(&Ts[row][c0]) : zero4();
+    const f32x4 t1 = hi_blk ? *reinterpret_cast<const f32x4*>(&Ts[row][c0 + 16]) : zero4();
+    const float tv[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+    float pv[8];
+    if constexpr (FWD) {
+      const f32x4 p0 = lo_blk ? *reinterpret_cast<const f32x4*>(&Ps[row][c0]) : zero4();
+      const f32x4 p1 = hi_blk ? *reinterpret_cast<const f32x4*>(&Ps[row][c0 + 16]) : zero4();
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int col = 32 * kk + kperm(fg, j);
-      const bool lower = col / 16 <= row / 16;
-      tv[j] = lower ? Ts[row][col] : 0.f;
-      if constexpr (FWD) pv[j] = lower ? Ps[row][col] : 0.f;
+      for (int j = 0; j < 4; ++j) {
+        pv[j] = p0[j];
+        pv[4 + j] = p1[j];
+      }
     }
     const Frag tf = split8(tv);
     tdst[e] = __builtin_bit_cast(u32x4, tf.hi);
