@@ -1199,17 +1199,18 @@ void k_scan_cols_split(int32_t n_first, const int32_t* __restrict__ cu, int32_t 
 // state = A state + B per (sequence, value head): A^T [d_k x d_k], state and
 // B [d_k x d_v], fp32 row-major.  grid N x Hv x d_v / 16; a workgroup owns 16
 // whole columns of one state (it reads them all before it writes any) and
-// stages A^T and those columns in LDS, every load in flight at once.  The
-// product runs on fp32 MFMA (16x16x4, fp32 products and sums): wave w takes
-// the 16-row tiles w, w + 4, ..; per 4-step slice of k, lane l supplies
-// A[16 t + l % 16][k + l / 16] (= A^T[k + l / 16][..], one conflict-free LDS
-// read) and column l % 16 of row k + l / 16 of the staged state, and holds
-// D[4 (l / 16) + i][l % 16] of the tile.
+// stages those columns in LDS, every load in flight at once.  The product
+// runs on fp32 MFMA (16x16x4, fp32 products and sums): wave w takes the
+// 16-row tiles w, w + 4, ..; per 4-step slice of k, lane l supplies
+// A[16 t + l % 16][k + l / 16] (= A^T[k + l / 16][..], read from memory into
+// registers up front) and column l % 16 of row k + l / 16 of the staged
+// state, and holds D[4 (l / 16) + i][l % 16] of the tile.  With 8 KiB of LDS
+// the combine leaves room for four preparation workgroups per CU beside it
+// in k_combine_intra.
 constexpr int kCombineThreads = 256;
 constexpr int kCombineCols = 16;
 template <int DK>
 struct CombineLds {
-  alignas(16) float as[DK * DK];
   alignas(16) float ms[DK * kCombineCols];
 };
 
@@ -1221,9 +1222,7 @@ __device__ __forceinline__ void combine_body(CombineLds<DK>& sm, int block, int 
                                              const float* __restrict__ At, const float* __restrict__ B,
                                              float* __restrict__ state) {
   constexpr int PER = DK * kCombineCols / kCombineThreads;   // staged column values per thread
-  constexpr int AV = DK * DK / 4 / kCombineThreads;          // 16-byte pieces of A^T per thread
   constexpr int TILES = DK / 16 / (kCombineThreads / kWave);  // row tiles per wave
-  float* as = sm.as;
   float* ms = sm.ms;
   const int groups = dv / kCombineCols;
   const int unit = xcd_cluster_remap(block, nblocks, groups);
@@ -1233,10 +1232,14 @@ __device__ __forceinline__ void combine_body(CombineLds<DK>& sm, int block, int 
   const int li = lane % 16, lk = lane / 16;
   float* st = state + head * DK * dv + c0;
   const float* bm = B + head * DK * dv + c0;
-  const f32x4* at = reinterpret_cast<const f32x4*>(At + head * DK * DK);
-  f32x4 av[AV];
+  const float* at = At + head * DK * DK;
+  // the wave's A operands straight from memory (A^T rows are 16 consecutive
+  // floats per tile: 64-byte pieces), every load in flight at once
+  float av[DK / 4][TILES];
 #pragma unroll
-  for (int i = 0; i < AV; ++i) av[i] = at[tid + kCombineThreads * i];
+  for (int k = 0; k < DK; k += 4)
+#pragma unroll
+    for (int t = 0; t < TILES; ++t) av[k / 4][t] = at[(k + lk) * DK + 16 * (wave + 4 * t) + li];
   float mv[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
@@ -1250,24 +1253,19 @@ __device__ __forceinline__ void combine_body(CombineLds<DK>& sm, int block, int 
     for (int i = 0; i < 4; ++i)
       acc[t][i] = bm[static_cast<int64_t>(16 * (wave + 4 * t) + 4 * lk + i) * dv + li];
 #pragma unroll
-  for (int i = 0; i < AV; ++i) reinterpret_cast<f32x4*>(as)[tid + kCombineThreads * i] = av[i];
-#pragma unroll
   for (int i = 0; i < PER; ++i) ms[tid + kCombineThreads * i] = mv[i];
   __syncthreads();
-#pragma unroll 4
+#pragma unroll
   for (int k = 0; k < DK; k += 4) {
     const float b = ms[(k + lk) * kCombineCols + li];
 #pragma unroll
-    for (int t = 0; t < TILES; ++t)
-      acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(as[(k + lk) * DK + 16 * (wave + 4 * t) + li], b, acc[t],
-                                                    0, 0, 0);
+    for (int t = 0; t < TILES; ++t) acc[t] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[k / 4][t], b, acc[t], 0, 0, 0);
   }
 #pragma unroll
   for (int t = 0; t < TILES; ++t)
 #pragma unroll
     for (int i = 0; i < 4; ++i) st[static_cast<int64_t>(16 * (wave + 4 * t) + 4 * lk + i) * dv + li] = acc[t][i];
 }
-
 template <int DK>
 __global__ __launch_bounds__(kCombineThreads)
 void k_state_combine(int32_t dv, const float* __restrict__ At, const float* __restrict__ B,
