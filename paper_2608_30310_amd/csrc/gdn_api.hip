@@ -93,12 +93,18 @@ template <typename TIn, int DK, bool FWD>
 gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, const void* q, const void* k,
                         const float* g, const float* beta, char* ws, hipStream_t stream) {
   if (p.num_slots == 0) return GDN_OK;
-  hipLaunchKernelGGL((k_intra<TIn, DK, FWD>), dim3(static_cast<uint32_t>(p.num_slots), s.num_v_heads),
-                     dim3(kThreads), 0, stream, cu, s.num_seqs, s.num_k_heads, s.num_v_heads,
-                     static_cast<const TIn*>(q), static_cast<const TIn*>(k), g, beta, s.scale,
-                     reinterpret_cast<u32x4*>(ws + p.off_K), reinterpret_cast<u32x4*>(ws + p.off_T),
-                     reinterpret_cast<float*>(ws + p.off_S),
-                     FWD ? reinterpret_cast<u32x4*>(ws + p.off_P) : nullptr);
+  const dim3 block(kThreads);
+  const auto args = [&](auto kernel, uint32_t heads_per_group) {
+    hipLaunchKernelGGL(kernel, dim3(static_cast<uint32_t>(p.num_slots), s.num_v_heads / heads_per_group), block, 0,
+                       stream, cu, s.num_seqs, s.num_k_heads, s.num_v_heads, static_cast<const TIn*>(q),
+                       static_cast<const TIn*>(k), g, beta, s.scale, reinterpret_cast<u32x4*>(ws + p.off_K),
+                       reinterpret_cast<u32x4*>(ws + p.off_T), reinterpret_cast<float*>(ws + p.off_S),
+                       FWD ? reinterpret_cast<u32x4*>(ws + p.off_P) : nullptr);
+  };
+  // tail replay: one workgroup per two value heads of a key head where the
+  // group allows (the key rows are loaded and K K^T formed once for both)
+  if (!FWD && (s.num_v_heads / s.num_k_heads) % 2 == 0) args(k_intra<TIn, DK, FWD, FWD ? 1 : 2>, 2);
+  else args(k_intra<TIn, DK, FWD, 1>, 1);
   return check_launch("intra launch");
 }
 

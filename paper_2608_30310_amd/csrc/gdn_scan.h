@@ -49,6 +49,14 @@ __device__ __forceinline__ void dma16(const void* src, lds_byte* dst) {
 
 __device__ __forceinline__ void wait_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// The same from `base + off`: a uniform base and a 32-bit lane offset, so the
+// load takes the scalar-base form and its address costs no 64-bit lane
+// arithmetic.  Offsets stay below 2^32: a chunk spans 64 rows of at most
+// 65535 heads x 128 x 4 bytes.
+__device__ __forceinline__ void dma16_at(const void* base, uint32_t off, lds_byte* dst) {
+  dma16(static_cast<const unsigned char*>(base) + off, dst);
+}
+
 
 // Byte offset of byte `byte_in_row` of row `row` in a row tile whose rows hold
 // ROW_BYTES / 16 pieces of 16 bytes, piece p of row R stored at p ^ (R % pieces).
@@ -68,8 +76,8 @@ __device__ __forceinline__ void dma_rows(const T* row0, int64_t row_stride, int 
   constexpr int rows_per_block = 1024 / ROW_BYTES;
   const int r = blk * rows_per_block + lane / pieces;
   const int p = (lane % pieces) ^ (r % pieces);
-  const T* src = row0 + min(r, rows - 1) * row_stride + p * (16 / static_cast<int>(sizeof(T)));
-  dma16(src, dst + blk * 1024);
+  const uint32_t stride_b = static_cast<uint32_t>(row_stride) * static_cast<uint32_t>(sizeof(T));
+  dma16_at(row0, static_cast<uint32_t>(min(r, rows - 1)) * stride_b + 16u * p, dst + blk * 1024);
 }
 
 // Element j (0..3) of four bf16 values packed in two dwords, as float.
@@ -140,7 +148,7 @@ template <typename L, typename TIn>
 __device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, lds_byte* base, int j, int lane) {
   if (j < L::kKJobs) {
     if constexpr (L::kSplit) {
-      dma16(c.krec + 1024 * j + 16 * lane, base + L::kOffK + 1024 * j);
+      dma16_at(c.krec + 1024 * j, 16u * lane, base + L::kOffK + 1024 * j);
     } else {
       // fragment j: keys for j < 4 d_k/32, then queries; the lane at position
       // `lane` (kslot order) takes 16 bytes of row 16 ti + r at column 32 kk +
@@ -150,23 +158,24 @@ __device__ __forceinline__ void dma_job(const ChunkSrc& c, int64_t vrow, lds_byt
       const int f = isq ? j - NKA : j;
       const int l = kslot_inv(lane);
       const int row = min(16 * (f / NK) + (l & 15), c.clen - 1);
-      const uint16_t* src = static_cast<const uint16_t*>(isq ? c.q0 : c.k0) + row * c.krow + 32 * (f % NK) + 8 * (l >> 4);
-      dma16(src, base + L::kOffK + 1024 * j);
+      const uint32_t krow_b = static_cast<uint32_t>(c.krow) * 2u;
+      dma16_at(static_cast<const uint16_t*>(isq ? c.q0 : c.k0) + 32 * (f % NK),
+               static_cast<uint32_t>(row) * krow_b + 16u * (l >> 4), base + L::kOffK + 1024 * j);
     }
   } else if (j < L::kKJobs + L::kTJobs) {
     const int t = j - L::kKJobs;
-    dma16(c.trec + 1024 * t + 16 * lane, base + L::kOffT + 1024 * t);
+    dma16_at(c.trec + 1024 * t, 16u * lane, base + L::kOffT + 1024 * t);
   } else if (j < L::kKJobs + L::kTJobs + L::kPJobs) {
     const int t = j - L::kKJobs - L::kTJobs;
-    dma16(c.prec + 1024 * t + 16 * lane, base + L::kOffP + 1024 * t);
+    dma16_at(c.prec + 1024 * t, 16u * lane, base + L::kOffP + 1024 * t);
   } else if (j < L::kKJobs + L::kTJobs + L::kPJobs + L::kVJobs) {
     // V rows; pad rows repeat the last row (their beta is 0, so they add nothing)
     dma_rows<L::kVRowBytes>(static_cast<const TIn*>(c.v0), vrow, c.clen, base + L::kOffV,
                             j - L::kKJobs - L::kTJobs - L::kPJobs, lane);
   } else if (j == L::kJobs - 2) {
-    dma16(c.srow + 16 * lane, base + L::kOffS);                    // scalars, bytes 0..1023
+    dma16_at(c.srow, 16u * lane, base + L::kOffS);                 // scalars, bytes 0..1023
   } else if (lane < 16) {
-    dma16(c.srow + 1024 + 16 * lane, base + L::kOffS + 1024);      // bytes 1024..1279
+    dma16_at(c.srow + 1024, 16u * lane, base + L::kOffS + 1024);   // bytes 1024..1279
   }
 }
 
@@ -714,15 +723,16 @@ constexpr int cols_wide_threads(int cols) { return cols / (16 * kWideTiles) * kW
 //                              identity start with V = 0, d_k columns -> a2
 // and k_state_combine forms A M' + M'' in state_out.  Each part is the
 // unsplit scan's arithmetic on its chunks.  The first half runs 32 columns
-// per workgroup (~1.9 us per chunk on MI355X with every CU busy), the second
-// 64 (~2.4 us: four waves read the chunk's operands from LDS), so the first
-// half takes the first round(n x 2.4 / 4.3) chunks.
+// per workgroup, the second 64 (four waves read the chunk's operands from LDS,
+// and the part starts later), so the first half takes the first
+// round(0.54 n) chunks: on MI355X at n = 52 and 26 the halves then end
+// closest together (28 of 52: the split scan 47.0 -> 46.3 us against 29).
 enum ScanPart { kWhole = 0, kFirstHalf = 1, kSecondHalf = 2 };
 struct SplitOut {
   float* m2;   // [N, Hv, d_k, d_v] second half from zero
   float* a2;   // [N, Hv, d_k, d_k] second half's transition, transposed (A^T)
 };
-__device__ __forceinline__ int split_point(int nch) { return (24 * nch + 21) / 43; }
+__device__ __forceinline__ int split_point(int nch) { return (27 * nch + 25) / 50; }
 
 // One column-split workgroup (block `block` of `nblocks`), LDS in `lds`, COLS
 // columns per workgroup, NC tiles of 16 columns per compute wave.  Waves 0 ..
@@ -1008,10 +1018,10 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
     for (int q = q0; q < q1; ++q) {
       if (q < L::kKJobs / 2) {
         const int j = 2 * q + h;
-        dma16(c.krec + 1024 * j + 16 * lane, dst + L::kOffK + 1024 * j);
+        dma16_at(c.krec + 1024 * j, 16u * lane, dst + L::kOffK + 1024 * j);
       } else if (q < (L::kKJobs + L::kTJobs) / 2) {
         const int j = 2 * (q - L::kKJobs / 2) + h;
-        dma16(c.trec + 1024 * j + 16 * lane, dst + L::kOffT + 1024 * j);
+        dma16_at(c.trec + 1024 * j, 16u * lane, dst + L::kOffT + 1024 * j);
       } else {
         // V rows; pad rows repeat the last row (their beta is 0, so they add nothing)
         dma_rows<L::kVRowBytes>(static_cast<const TIn*>(c.v0), vrow, c.clen, dst + L::kOffV,
@@ -1019,8 +1029,8 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
       }
     }
     if (q1 == kHalf) {
-      if (h == 0) dma16(c.srow + 16 * lane, dst + L::kOffS);                          // bytes 0..1023
-      else if (lane < 16) dma16(c.srow + 1024 + 16 * lane, dst + L::kOffS + 1024);    // 1024..1279
+      if (h == 0) dma16_at(c.srow, 16u * lane, dst + L::kOffS);                       // bytes 0..1023
+      else if (lane < 16) dma16_at(c.srow + 1024, 16u * lane, dst + L::kOffS + 1024); // 1024..1279
     }
   };
 
