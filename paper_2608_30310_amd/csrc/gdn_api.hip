@@ -102,8 +102,17 @@ gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, co
                        FWD ? reinterpret_cast<u32x4*>(ws + p.off_P) : nullptr);
   };
   // tail replay: one workgroup per two value heads of a key head where the
-  // group allows (the key rows are loaded and K K^T formed once for both)
-  if (!FWD && (s.num_v_heads / s.num_k_heads) % 2 == 0) args(k_intra<TIn, DK, FWD, FWD ? 1 : 2>, 2);
+  // group allows and one workgroup per head would take more than one round of
+  // the chip (seven per CU): the key rows are loaded and K K^T formed once for
+  // both heads, which saves work in a throughput batch, while a grid that fits
+  // at once finishes sooner with a head per workgroup
+  int dev = 0, cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+    return fail(GDN_ERR_HIP, "querying the device");
+  const bool pair = !FWD && (s.num_v_heads / s.num_k_heads) % 2 == 0 &&
+                    p.num_slots * s.num_v_heads > 7 * static_cast<int64_t>(cus);
+  if (pair) args(k_intra<TIn, DK, FWD, FWD ? 1 : 2>, 2);
   else args(k_intra<TIn, DK, FWD, 1>, 1);
   return check_launch("intra launch");
 }

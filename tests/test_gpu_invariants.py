@@ -193,6 +193,23 @@ def test_whole_head_and_column_kernels_agree():
         assert rel.item() <= 1e-3   # bf16 outputs: one rounding step apart at most
 
 
+def test_two_heads_per_preparation_workgroup_bitwise():
+    # 64 sequences at 32 value heads (two per key head): the tail's chunk
+    # preparation grid exceeds one round of the chip, so each workgroup
+    # prepares both value heads of a key head; single sequences prepare one
+    # head per workgroup.  The per-head arithmetic is the same, and the wide
+    # and 32-wide scans agree bit for bit, so the states do too.
+    shape = synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16")
+    lens = [1 + (97 * i) % 300 for i in range(64)]
+    seqs = [_seq(i, n, shape=shape) for i, n in enumerate(lens)]
+    x = device_inputs(synth.pack(seqs))
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    for i in (0, 17, 63):
+        xi = device_inputs(synth.pack([seqs[i]]))
+        sti = gdn.tail_replay(xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"], xi["cu_host"])
+        assert torch.equal(st[i:i + 1], sti), f"sequence {i} (length {lens[i]})"
+
+
 @pytest.mark.parametrize("case", ["one", "ragged", "wide", "ragged_d64", "ragged_dk64", "ragged_dv64", "split",
                                   "split_no_suffix"])
 def test_replay_forward_equals_the_two_calls_bitwise(case):
