@@ -94,7 +94,7 @@ gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, co
                         const float* g, const float* beta, char* ws, hipStream_t stream) {
   if (p.num_slots == 0) return GDN_OK;
   const dim3 block(kThreads);
-  const auto args = [&](auto kernel, uint32_t heads_per_group) {
+  const auto launch = [&](auto kernel, uint32_t heads_per_group) {
     hipLaunchKernelGGL(kernel, dim3(static_cast<uint32_t>(p.num_slots), s.num_v_heads / heads_per_group), block, 0,
                        stream, cu, s.num_seqs, s.num_k_heads, s.num_v_heads, static_cast<const TIn*>(q),
                        static_cast<const TIn*>(k), g, beta, s.scale, reinterpret_cast<u32x4*>(ws + p.off_K),
@@ -112,8 +112,8 @@ gdn_status launch_intra(const gdn_shape& s, const Plan& p, const int32_t* cu, co
     return fail(GDN_ERR_HIP, "querying the device");
   const bool pair = !FWD && (s.num_v_heads / s.num_k_heads) % 2 == 0 &&
                     p.num_slots * s.num_v_heads > 7 * static_cast<int64_t>(cus);
-  if (pair) args(k_intra<TIn, DK, FWD, FWD ? 1 : 2>, 2);
-  else args(k_intra<TIn, DK, FWD, 1>, 1);
+  if (pair) launch(k_intra<TIn, DK, FWD, FWD ? 1 : 2>, 2);
+  else launch(k_intra<TIn, DK, FWD, 1>, 1);
   return check_launch("intra launch");
 }
 
