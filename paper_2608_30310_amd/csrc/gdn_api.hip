@@ -186,12 +186,36 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
                        static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in,
                        static_cast<TIn*>(o), state_out);
   } else if constexpr (kWide) {
-    // a whole head per workgroup (128 columns, four compute waves) where d_v allows
+    // a whole head per workgroup (128 columns, four compute waves) where d_v
+    // allows, two workgroups per CU.  When the batch's last round of that grid
+    // would be partly empty and its sequences fit on the chip at one 64-column
+    // workgroup per CU, those sequences (the shortest, in longest-first order)
+    // run in the one-tile scan after it instead: a two-tile chain left alone
+    // on a SIMD still takes longer per chunk than a one-tile chain.
     constexpr int kCols = DV >= 128 ? 128 : 64;
-    const uint32_t wide_groups = static_cast<uint32_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kCols);
-    hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK, kCols>), dim3(wide_groups), dim3(cols_wide_threads(kCols)), 0,
-                       stream, cu, p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
-                       static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, state_out);
+    const int64_t per_seq = static_cast<int64_t>(s.num_v_heads) * (s.d_v / kCols);
+    const int64_t rem = static_cast<int64_t>(s.num_seqs) * per_seq % (2 * static_cast<int64_t>(cus));
+    int32_t peel = 0;
+    if (rem > 0 && s.num_seqs <= kMaxOrderedSeqs) {
+      peel = static_cast<int32_t>((rem + per_seq - 1) / per_seq);
+      if (peel >= s.num_seqs || static_cast<int64_t>(peel) * s.num_v_heads * (s.d_v / kSplitCols2) > cus) peel = 0;
+    }
+    const int32_t n_wide = s.num_seqs - peel;
+    hipLaunchKernelGGL((k_scan_cols_wide<TIn, DK, kCols>), dim3(static_cast<uint32_t>(n_wide * per_seq)),
+                       dim3(cols_wide_threads(kCols)), 0, stream, cu, p.order, s.num_k_heads, s.num_v_heads, s.d_v,
+                       static_cast<const TIn*>(v), static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw,
+                       state_out);
+    if (peel > 0) {
+      if ((st = check_launch("scan launch")) != GDN_OK) return st;
+      SeqOrder po;
+      po.n = peel;
+      for (int32_t i = 0; i < peel; ++i) po.seq[i] = p.order.n > 0 ? p.order.seq[n_wide + i] : n_wide + i;
+      hipLaunchKernelGGL((k_scan_cols_peel<TIn, DK>), dim3(static_cast<uint32_t>(peel) * s.num_v_heads *
+                                                           (s.d_v / kSplitCols2)),
+                         dim3((kSplitCols2 / 16 + 1) * kWave), 0, stream, cu, po, s.num_k_heads, s.num_v_heads, s.d_v,
+                         static_cast<const TIn*>(v), static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw,
+                         Sw, state_out);
+    }
   } else {
     hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
                        dim3(head_threads(DV)), 0, stream, cu, p.order, s.num_k_heads, s.num_v_heads,

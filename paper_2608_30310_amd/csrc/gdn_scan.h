@@ -1177,6 +1177,24 @@ void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int3
                                                                   nullptr, nullptr, state_out, SplitOut{}, &order);
 }
 
+// The last sequences of a wide batch, where the wide scan's last round would
+// be partly empty (see launch_scan): 64 columns per workgroup, one 16-column
+// tile per compute wave beside a DMA wave (the chains of the split scan's
+// second half, which finish a chunk sooner than a two-tile wave), grid
+// P x Hv x d_v / 64 over the P sequences `order` names.
+template <typename TIn, int DK>
+__global__ __launch_bounds__((kSplitCols2 / 16 + 1) * kWave)
+void k_scan_cols_peel(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
+                      const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
+                      const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                      const float* __restrict__ Sw, float* __restrict__ state_out) {
+  using L = ColsLds<TIn, DK, false, kSplitCols2>;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[L::kBuffers * L::kBytes];
+  scan_cols_body<TIn, DK, false, kSplitCols2, kWhole, 1, true>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv,
+                                                               dv, v, kin, qin, Kw, Tw, Sw, nullptr, nullptr,
+                                                               nullptr, state_out, SplitOut{}, &order);
+}
+
 // Tail replay in two halves, one launch: blocks [0, n_first) run the first
 // half kSplitCols1 = 32 columns wide (grid N x Hv x d_v / 32; waves 3 and 4
 // only take part in the barriers), the rest the second half and its
