@@ -186,12 +186,23 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
                        static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in,
                        static_cast<TIn*>(o), state_out);
   } else if constexpr (kWide) {
-    // a whole head per workgroup (128 columns, four compute waves) where d_v
-    // allows, two workgroups per CU.  When the batch's last round of that grid
-    // would be partly empty and its sequences fit on the chip at one 64-column
-    // workgroup per CU, those sequences (the shortest, in longest-first order)
-    // run in the one-tile scan after it instead: a two-tile chain left alone
-    // on a SIMD still takes longer per chunk than a one-tile chain.
+    // A batch whose 64-column one-tile grid takes at most three rounds of the
+    // chip (one workgroup per CU) runs in it: its chains finish a chunk in
+    // ~1.45 us against ~3.9 us for a lone wide workgroup per CU (at 3, 8 and
+    // 12 sequences of 32 heads: 178 -> 88, 196 -> 182, 283 -> 270 us).
+    const int64_t groups64 = static_cast<int64_t>(s.num_seqs) * s.num_v_heads * (s.d_v / kSplitCols2);
+    if (groups64 <= 3 * static_cast<int64_t>(cus)) {
+      hipLaunchKernelGGL((k_scan_cols_64<TIn, DK>), dim3(static_cast<uint32_t>(groups64)),
+                         dim3((kSplitCols2 / 16 + 1) * kWave), 0, stream, cu, p.order, s.num_k_heads, s.num_v_heads,
+                         s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw,
+                         Tw, Sw, state_out);
+      return check_launch("scan launch");
+    }
+    // Otherwise a whole head per workgroup (128 columns, four compute waves)
+    // where d_v allows, two workgroups per CU.  When the last round of that
+    // grid would be partly empty and its sequences fit on the chip at one
+    // 64-column workgroup per CU, those sequences (the shortest, in
+    // longest-first order) run in the one-tile scan after it instead.
     constexpr int kCols = DV >= 128 ? 128 : 64;
     const int64_t per_seq = static_cast<int64_t>(s.num_v_heads) * (s.d_v / kCols);
     const int64_t rem = static_cast<int64_t>(s.num_seqs) * per_seq % (2 * static_cast<int64_t>(cus));
@@ -210,7 +221,7 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
       SeqOrder po;
       po.n = peel;
       for (int32_t i = 0; i < peel; ++i) po.seq[i] = p.order.n > 0 ? p.order.seq[n_wide + i] : n_wide + i;
-      hipLaunchKernelGGL((k_scan_cols_peel<TIn, DK>), dim3(static_cast<uint32_t>(peel) * s.num_v_heads *
+      hipLaunchKernelGGL((k_scan_cols_64<TIn, DK>), dim3(static_cast<uint32_t>(peel) * s.num_v_heads *
                                                            (s.d_v / kSplitCols2)),
                          dim3((kSplitCols2 / 16 + 1) * kWave), 0, stream, cu, po, s.num_k_heads, s.num_v_heads, s.d_v,
                          static_cast<const TIn*>(v), static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw,

@@ -1177,14 +1177,15 @@ void k_scan_cols_wide(const int32_t* __restrict__ cu, const SeqOrder order, int3
                                                                   nullptr, nullptr, state_out, SplitOut{}, &order);
 }
 
-// The last sequences of a wide batch, where the wide scan's last round would
-// be partly empty (see launch_scan): 64 columns per workgroup, one 16-column
-// tile per compute wave beside a DMA wave (the chains of the split scan's
-// second half, which finish a chunk sooner than a two-tile wave), grid
-// P x Hv x d_v / 64 over the P sequences `order` names.
+// Tail replay of bf16 inputs, 64 columns per workgroup: one 16-column tile per
+// compute wave beside a DMA wave (the chains of the split scan's second half,
+// which finish a chunk sooner than the wide scan's two-tile waves), grid
+// P x Hv x d_v / 64 over the P sequences `order` names (all of them when its
+// n is 0).  Used for batches whose grid takes at most three rounds of the
+// chip, and for the sequences of a wide grid's partly empty last round.
 template <typename TIn, int DK>
 __global__ __launch_bounds__((kSplitCols2 / 16 + 1) * kWave)
-void k_scan_cols_peel(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
+void k_scan_cols_64(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
                       const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                       const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                       const float* __restrict__ Sw, float* __restrict__ state_out) {

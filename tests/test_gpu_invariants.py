@@ -193,13 +193,14 @@ def test_whole_head_and_column_kernels_agree():
         assert rel.item() <= 1e-3   # bf16 outputs: one rounding step apart at most
 
 
-@pytest.mark.parametrize("nseq", [12, 36])
-def test_peeled_last_round_bitwise(nseq):
-    # 36 sequences at 32 value heads: 1152 wide-scan workgroups, two per CU,
-    # leave the last round a quarter full on MI355X, so the four shortest
-    # sequences run in the one-tile scan after the wide one (12 sequences, 384
-    # workgroups, run wide alone); every sequence's state must be bitwise that
-    # of its own call (the one-tile and two-tile chains run the same products)
+@pytest.mark.parametrize("nseq", [3, 12, 36])
+def test_one_tile_and_wide_batches_bitwise(nseq):
+    # 3 and 12 sequences at 32 value heads run in the 64-column one-tile scan
+    # (at most three rounds of MI355X's 256 CUs); 36 run wide (1152
+    # workgroups, two per CU), whose last round would be a quarter full, so
+    # the four shortest run in the one-tile scan after it.  Every sequence's
+    # state must be bitwise that of its own call (the one-tile, two-tile and
+    # 32-column chains run the same products).
     shape = synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16")
     lens = [64 + (37 * i) % 200 for i in range(nseq)]
     seqs = [_seq(i, n, shape=shape) for i, n in enumerate(lens)]
