@@ -228,10 +228,39 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
                          Sw, state_out);
     }
   } else {
-    hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(s.num_seqs) * s.num_v_heads),
+    // a whole head per workgroup, one per CU.  With outputs, when the grid's
+    // last round would be partly empty and its sequences (the shortest, in
+    // longest-first order) fit in two rounds of the 32-column scan with
+    // output waves, they run in that after the whole-head grid (12 and 36
+    // sequences of 32 heads, 16 chunks: 216 -> 205 and 557 -> 545 us).
+    int32_t peel = 0;
+    if constexpr (FWD) {
+      const int64_t rem = static_cast<int64_t>(s.num_seqs) * s.num_v_heads % cus;
+      if (rem > 0 && s.num_seqs <= kMaxOrderedSeqs) {
+        peel = static_cast<int32_t>((rem + s.num_v_heads - 1) / s.num_v_heads);
+        if (peel >= s.num_seqs ||
+            static_cast<int64_t>(peel) * s.num_v_heads * (s.d_v / kColsPerGroup) > 2 * static_cast<int64_t>(cus))
+          peel = 0;
+      }
+    }
+    const int32_t n_head = s.num_seqs - peel;
+    hipLaunchKernelGGL((k_scan_head<TIn, DK, DV, FWD>), dim3(static_cast<uint32_t>(n_head) * s.num_v_heads),
                        dim3(head_threads(DV)), 0, stream, cu, p.order, s.num_k_heads, s.num_v_heads,
                        static_cast<const TIn*>(v), static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw,
                        Pw, state_in, static_cast<TIn*>(o), state_out);
+    if constexpr (FWD) {
+      if (peel > 0) {
+        if ((st = check_launch("scan launch")) != GDN_OK) return st;
+        SeqOrder po;
+        po.n = peel;
+        for (int32_t i = 0; i < peel; ++i) po.seq[i] = p.order.n > 0 ? p.order.seq[n_head + i] : n_head + i;
+        hipLaunchKernelGGL((k_scan_cols_fwd_peel<TIn, DK>),
+                           dim3(static_cast<uint32_t>(peel) * s.num_v_heads * (s.d_v / kColsPerGroup)),
+                           dim3(cols_threads(true, sizeof(TIn) == 4)), 0, stream, cu, po, s.num_k_heads,
+                           s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),
+                           static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in, static_cast<TIn*>(o), state_out);
+      }
+    }
   }
   return check_launch("scan launch");
 }

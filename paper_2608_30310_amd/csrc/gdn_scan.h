@@ -962,7 +962,8 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
                                                    const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                                                    const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
                                                    const float* __restrict__ state_in, TIn* __restrict__ o,
-                                                   float* __restrict__ state_out) {
+                                                   float* __restrict__ state_out,
+                                                   const SeqOrder* order = nullptr) {
   using CL = ColsOutLayout<TIn, DK, TILES>;
   using L = typename CL::L;
   constexpr bool SPLIT = L::kSplit;
@@ -990,7 +991,7 @@ __device__ __forceinline__ void scan_cols_out_body(lds_byte* lds_l, int block, i
   // key head, are adjacent and one cluster (same XCD, shared records in its L2)
   const int unit = xcd_cluster_remap(block, nblocks, ngroups * (hv / hk));
   const int col0 = COLS * (unit % ngroups);
-  const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk);
+  const ScanUnit u = scan_unit(cu, unit / (ngroups * hv), (unit / ngroups) % hv, hv, hk, order);
   const int colw = col0 + 16 * tile;
   const int64_t vrow = static_cast<int64_t>(hv) * dv;
   unsigned char* xd = (unsigned char*)(lds_l + CL::kOffX + tile * CL::kTileBytes);
@@ -1161,6 +1162,21 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
     scan_cols_body<TIn, DK, false>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin, Kw, Tw, Sw, Pw,
                                    state_in, o, state_out);
   }
+}
+
+// The forward (with outputs) of the sequences peeled off a whole-head grid's
+// partly empty last round (see launch_scan): the 32-column scan with output
+// waves over the sequences `order` names (grid P x Hv x d_v / 32).
+template <typename TIn, int DK>
+__global__ __launch_bounds__(cols_threads(true, sizeof(TIn) == 4)) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_scan_cols_fwd_peel(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
+                          const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
+                          const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
+                          const float* __restrict__ Sw, const u32x4* __restrict__ Pw,
+                          const float* __restrict__ state_in, TIn* __restrict__ o, float* __restrict__ state_out) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[ColsOutLayout<TIn, DK>::kBytes];
+  scan_cols_out_body<TIn, DK>((lds_byte*)lds, blockIdx.x, gridDim.x, cu, hk, hv, dv, v, kin, qin, Kw, Tw, Sw, Pw,
+                              state_in, o, state_out, &order);
 }
 
 // The wide column scan, tail replay only (grid N x Hv x d_v / COLS).

@@ -212,6 +212,33 @@ def test_one_tile_and_wide_batches_bitwise(nseq):
         assert torch.equal(st[i:i + 1], sti), f"sequence {i} (length {lens[i]})"
 
 
+@pytest.mark.parametrize("nseq", [12, 36])
+def test_forward_batches_with_a_peeled_last_round(nseq):
+    # 12 and 36 sequences at 32 value heads run the forward on the whole-head
+    # kernel (384 and 1152 workgroups, one per CU); the last round would hold
+    # 128 of 256, so the four shortest sequences run in the 32-column scan
+    # with output waves after it.  States agree bit for bit with each
+    # sequence's own call (same products, same order); outputs to within one
+    # bf16 rounding (the whole-head kernel sums the output's two terms in
+    # another order).
+    shape = synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16")
+    lens = [64 + (37 * i) % 200 for i in range(nseq)]
+    seqs = [_seq(i, n, shape=shape) for i, n in enumerate(lens)]
+    p = synth.pack(seqs)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    o, st_f = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                                state_in=st)
+    for i in range(nseq):
+        xi = device_inputs(synth.pack([seqs[i]]))
+        oi, sfi = gdn.chunk_forward(xi["q"], xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"],
+                                    xi["cu_host"], state_in=st[i:i + 1].contiguous())
+        assert torch.equal(st_f[i:i + 1], sfi), f"sequence {i} (length {lens[i]})"
+        a, b = int(p.cu_seqlens[i]), int(p.cu_seqlens[i + 1])
+        rel = (o[a:b].float() - oi.float()).norm() / oi.float().norm()
+        assert rel.item() <= 1e-3, f"sequence {i} (length {lens[i]})"
+
+
 def test_two_heads_per_preparation_workgroup_bitwise():
     # 64 sequences at 32 value heads (two per key head): the tail's chunk
     # preparation grid exceeds one round of the chip, so each workgroup
