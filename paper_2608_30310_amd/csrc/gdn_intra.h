@@ -61,17 +61,22 @@ template <typename TIn, int DK, bool FWD, int HPW = 1>
 struct IntraLds {
   static_assert(HPW == 1 || (HPW == 2 && !FWD), "two value heads per workgroup for tail replay only");
   static constexpr bool kSplit = sizeof(TIn) == 4;
-  static constexpr int KP = DK + 8;                 // padded LDS row (bf16 elements)
+  // Row pitches are an odd multiple of 32 bytes: 16-byte reads of 16
+  // consecutive rows at one column (K K^T operands, record rows) are then
+  // free of bank conflicts on gfx950, where pitches of 16 or 48 bytes past a
+  // multiple of 64 cost 4 conflict cycles per read (measured with
+  // SQ_LDS_BANK_CONFLICT).
+  static constexpr int KP = DK + 16;                // padded LDS row (bf16 elements)
   static constexpr int NL = kSplit ? 2 : 1;         // hi (and lo) copies
-  static constexpr int AP = kChunk + 4;             // fp32 row pitch of A, T and P
+  static constexpr int AP = kChunk + 8;             // fp32 row pitch of A, T and P
   // A takes the keys' place: every read of the key tile (the operands of
   // K K^T and of the K record) is issued and waited for before the first
   // element of A is written.  Likewise P takes the queries' place.  And
   // T = (I + A)^-1 is formed in A's place: every step of the inversion reads
   // the blocks of A it needs before it writes the T block that replaces one of
   // them, and never reads that A block again.  Sizes (bf16, d_k = 128): tail
-  // replay of two value heads 36 KiB (four workgroups per CU), of one 18 KiB,
-  // forward 35 KiB (four).
+  // replay of two value heads 37 KiB (four workgroups per CU), of one 18.5
+  // KiB (eight), forward 36.5 KiB (four).
   union {
     alignas(16) uint16_t Ks[NL][kChunk][KP];
     alignas(16) float As[HPW][kChunk][AP];          // A (strictly lower), then T = (I + A)^-1
@@ -399,7 +404,7 @@ __device__ __forceinline__ void intra_body(IntraLds<TIn, DK, FWD, HPW>& sm, int 
     const int row = 16 * ti + fr;
     // the lane's elements j < 4 are columns 32 kk + 4 fg .. + 3 (column block
     // 2 kk) and j >= 4 the same 16 columns further (block 2 kk + 1): two
-    // 16-byte reads, conflict-free over each 16 lanes (rows 68 floats apart);
+    // 16-byte reads, conflict-free (rows 72 floats apart);
     // blocks above the diagonal are zero
     const int c0 = 32 * kk + 4 * fg;
     const bool lo_blk = 2 * kk <= ti, hi_blk = 2 * kk + 1 <= ti;
