@@ -180,9 +180,20 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
       return check_launch("scan launch");
     }
   }
+  // fp32 inputs with outputs: a grid that does not fit takes the 32-column scan
+  // over as many rounds as it needs, longest first.  The whole-head kernel's
+  // eight waves (two per SIMD) cannot hold fp32 operands and spill: at 3, 16
+  // and 36 sequences of 32 heads (1024 tokens) its forward scan took 213, 642
+  // and 1391 us against 113, 566 and 1233-1260 us in this form.
+  constexpr bool kColsOut = FWD && sizeof(TIn) == 4;
   if (fits) {
     hipLaunchKernelGGL((k_scan_cols<TIn, DK, FWD>), dim3(col_groups), dim3(cols_threads(FWD, sizeof(TIn) == 4)), 0,
                        stream, cu, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
+                       static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in,
+                       static_cast<TIn*>(o), state_out);
+  } else if constexpr (kColsOut) {
+    hipLaunchKernelGGL((k_scan_cols_out_ord<TIn, DK>), dim3(col_groups), dim3(cols_threads(true, true)), 0, stream,
+                       cu, p.order, s.num_k_heads, s.num_v_heads, s.d_v, static_cast<const TIn*>(v),
                        static_cast<const TIn*>(k), static_cast<const TIn*>(q), Kw, Tw, Sw, Pw, state_in,
                        static_cast<TIn*>(o), state_out);
   } else if constexpr (kWide) {
@@ -254,7 +265,7 @@ gdn_status launch_scan(const gdn_shape& s, const Plan& p, const int32_t* cu, con
         SeqOrder po;
         po.n = peel;
         for (int32_t i = 0; i < peel; ++i) po.seq[i] = p.order.n > 0 ? p.order.seq[n_head + i] : n_head + i;
-        hipLaunchKernelGGL((k_scan_cols_fwd_peel<TIn, DK>),
+        hipLaunchKernelGGL((k_scan_cols_out_ord<TIn, DK>),
                            dim3(static_cast<uint32_t>(peel) * s.num_v_heads * (s.d_v / kColsPerGroup)),
                            dim3(cols_threads(true, sizeof(TIn) == 4)), 0, stream, cu, po, s.num_k_heads,
                            s.num_v_heads, s.d_v, static_cast<const TIn*>(v), static_cast<const TIn*>(k),

@@ -1164,12 +1164,14 @@ void k_scan_cols(const int32_t* __restrict__ cu, int32_t hk, int32_t hv, int32_t
   }
 }
 
-// The forward (with outputs) of the sequences peeled off a whole-head grid's
-// partly empty last round (see launch_scan): the 32-column scan with output
-// waves over the sequences `order` names (grid P x Hv x d_v / 32).
+// The 32-column scan with output waves over the P sequences `order` names
+// (all of them, in index order, when its n is 0; grid P x Hv x d_v / 32, any
+// number of rounds): the forward of the sequences peeled off a whole-head
+// grid's partly empty last round, and of fp32 batches that do not fit on the
+// chip (see launch_scan).
 template <typename TIn, int DK>
 __global__ __launch_bounds__(cols_threads(true, sizeof(TIn) == 4)) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void k_scan_cols_fwd_peel(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
+void k_scan_cols_out_ord(const int32_t* __restrict__ cu, const SeqOrder order, int32_t hk, int32_t hv, int32_t dv,
                           const TIn* __restrict__ v, const TIn* __restrict__ kin, const TIn* __restrict__ qin,
                           const u32x4* __restrict__ Kw, const u32x4* __restrict__ Tw,
                           const float* __restrict__ Sw, const u32x4* __restrict__ Pw,

@@ -239,6 +239,28 @@ def test_forward_batches_with_a_peeled_last_round(nseq):
         assert rel.item() <= 1e-3, f"sequence {i} (length {lens[i]})"
 
 
+def test_fp32_forward_beyond_the_chip_bitwise():
+    # fp32 inputs with outputs: 72 varlen sequences x 4 heads need 1152
+    # 32-column workgroups, more than the chip holds, and run in that form over
+    # several rounds, longest first; single sequences fit and run the same
+    # body.  States and outputs agree bit for bit.
+    shape = synth.Shape(hk=2, hv=4, dk=128, dv=128, dtype="f32")
+    lens = [1 + (37 * i) % 200 for i in range(72)]
+    seqs = [_seq(i, n, shape=shape) for i, n in enumerate(lens)]
+    p = synth.pack(seqs)
+    x = device_inputs(p)
+    st = gdn.tail_replay(x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"])
+    o, st_f = gdn.chunk_forward(x["q"], x["k"], x["v"], x["g"], x["beta"], x["cu"], x["cu_host"],
+                                state_in=st)
+    for i in (0, 5, 40, 71):
+        xi = device_inputs(synth.pack([seqs[i]]))
+        oi, sfi = gdn.chunk_forward(xi["q"], xi["k"], xi["v"], xi["g"], xi["beta"], xi["cu"],
+                                    xi["cu_host"], state_in=st[i:i + 1].contiguous())
+        a, b = int(p.cu_seqlens[i]), int(p.cu_seqlens[i + 1])
+        assert torch.equal(o[a:b], oi), f"sequence {i} (length {lens[i]})"
+        assert torch.equal(st_f[i:i + 1], sfi), f"sequence {i} (length {lens[i]})"
+
+
 def test_two_heads_per_preparation_workgroup_bitwise():
     # 64 sequences at 32 value heads (two per key head): the tail's chunk
     # preparation grid exceeds one round of the chip, so each workgroup
