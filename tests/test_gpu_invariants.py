@@ -212,16 +212,17 @@ def test_one_tile_and_wide_batches_bitwise(nseq):
         assert torch.equal(st[i:i + 1], sti), f"sequence {i} (length {lens[i]})"
 
 
-@pytest.mark.parametrize("nseq", [12, 36])
-def test_forward_batches_with_a_peeled_last_round(nseq):
+@pytest.mark.parametrize("nseq,d", [(12, 128), (36, 128), (12, 64)])
+def test_forward_batches_with_a_peeled_last_round(nseq, d):
     # 12 and 36 sequences at 32 value heads run the forward on the whole-head
     # kernel (384 and 1152 workgroups, one per CU); the last round would hold
     # 128 of 256, so the four shortest sequences run in the 32-column scan
     # with output waves after it.  States agree bit for bit with each
     # sequence's own call (same products, same order); outputs to within one
     # bf16 rounding (the whole-head kernel sums the output's two terms in
-    # another order).
-    shape = synth.Shape(hk=16, hv=32, dk=128, dv=128, dtype="bf16")
+    # another order).  At d = 64 the same holds with two 32-column groups per
+    # head.
+    shape = synth.Shape(hk=16, hv=32, dk=d, dv=d, dtype="bf16")
     lens = [64 + (37 * i) % 200 for i in range(nseq)]
     seqs = [_seq(i, n, shape=shape) for i, n in enumerate(lens)]
     p = synth.pack(seqs)
